@@ -1,0 +1,319 @@
+#!/usr/bin/env python3
+"""Throughput of the DP-masked linear path on one MI355X.
+
+Default workload: one step = the whole hot path for one Llama-3.2-3B-shaped
+layer at a 128-token prefill: for each projection group (QKV 3072->5120,
+O 3072->3072, gate/up 3072->16384, down 8192->3072) noise + mask (one kernel)
+and the GEMM with the fused unmask epilogue (one kernel).  Weights are bf16
+~ N(0, 0.02^2), activations float32 ~ N(0, 1), Gaussian mechanism (Prop. 2)
+with Delta = 1, eps = 1; the corrections eta W^T are precomputed outside the
+timed region (the paper's offline step) and reported separately.  Steps cycle
+through 8 distinct weight sets so the 201 MB per layer is streamed from HBM,
+not the 256 MB MALL.  --workload selects the other shapes: the single float32
+projection, the 28-layer Llama stack at 512 tokens, the 36-layer Qwen3-4B stack
+at 1024 tokens, and Qwen3-4B decode steps (M tokens at position 1024 of a
+2048-position correction bank).
+
+Prints one JSON line.  Fields beyond the common contract: ``roofline`` (the
+GEMM + unmask kernel, timed per launch with HIP events on its stream),
+``cpu_baseline`` (the CPU oracle on a bounded sample of the same workload),
+``modes`` (other precision modes), ``correction_ms`` (offline precompute).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "masked-linear TFLOP/s (noise+mask+GEMM+unmask) and % MFMA/HBM roofline"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFS = 2500.0
+FP32_PEAK_TFS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3b-layer-m128", choices=WORKLOADS)
+    ap.add_argument("--prec", default="bf16x3", choices=["bf16x3", "bf16", "f32"])
+    ap.add_argument("--mech", default="gaussian", choices=["gaussian", "laplace", "none"])
+    ap.add_argument("--eps", type=float, default=1.0)
+    ap.add_argument("--delta", type=float, default=1.0)
+    ap.add_argument("--weight-sets", type=int, default=8)
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
+    ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle baseline sample")
+    return ap.parse_args()
+
+
+WORKLOADS = ["llama3b-layer-m128", "single-fp32-m32", "llama3b-28l-m512", "qwen3-4b-36l-m1024",
+             "qwen3-4b-decode-m1", "qwen3-4b-decode-m4", "qwen3-4b-decode-m16", "qwen3-4b-decode-m64"]
+DECODE_POS = 1024  # decode position t: rows [t, t+M) of the 2048-position correction bank
+
+
+def workload_spec(WL, name):
+    """(projections, tokens, layers per step, weight sets, weight dtype, bank rows, row0)."""
+    if name == "single-fp32-m32":
+        c = WL.SINGLE_FP32
+        return [WL.Projection("single", c["K"], c["N"], 0)], c["M"], 1, 8, "f32", 0, 0
+    if name == "llama3b-layer-m128":
+        return WL.LLAMA_3B.projections(), 128, 1, 8, "bf16", 0, 0
+    if name == "llama3b-28l-m512":
+        return WL.LLAMA_3B.projections(), 512, WL.LLAMA_3B.layers, 1, "bf16", 0, 0
+    if name == "qwen3-4b-36l-m1024":
+        return WL.QWEN3_4B.projections(), 1024, WL.QWEN3_4B.layers, 1, "bf16", 0, 0
+    if name.startswith("qwen3-4b-decode-m"):
+        m = int(name.rsplit("m", 1)[1])
+        return WL.QWEN3_4B.projections(), m, WL.QWEN3_4B.layers, 1, "bf16", 2048, DECODE_POS
+    raise ValueError(name)
+
+
+class Path:
+    """Device buffers of one workload: per layer (or weight set) and projection
+    group, the weights, the precomputed correction rows and the outputs."""
+
+    def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets):
+        self.torch, self.sp = torch, sp
+        self.prec, self.mech, self.delta, self.eps = prec, mech, delta, eps
+        (self.projs, self.M, self.layers_per_step, nsets, self.w_dtype, bank_rows,
+         self.row0) = workload_spec(WL, name)
+        if self.layers_per_step == 1 and weight_sets:
+            nsets = weight_sets
+        self.nsets = nsets if self.layers_per_step == 1 else 1
+        nlayers = self.layers_per_step * self.nsets
+        dev = "cuda"
+        M = self.M
+        g = torch.Generator(device=dev)
+        g.manual_seed(1)
+        wt = sp.SPLITEE_F32 if self.w_dtype == "f32" else sp.SPLITEE_BF16
+        self.wt = wt
+        self.X, self.Xt, self.Y, self.ws = [], [], [], []
+        for p in self.projs:
+            self.X.append(torch.randn((M, p.K), generator=g, device=dev, dtype=torch.float32))
+            planes = 3 if prec == sp.SPLITEE_PREC_BF16X3 else 1
+            dt = torch.float32 if prec == sp.SPLITEE_PREC_F32 else torch.int16
+            self.Xt.append(torch.empty((planes, M, p.K), dtype=dt, device=dev))
+            self.Y.append(torch.empty((M, p.N), dtype=torch.float32, device=dev))
+            self.ws.append(sp.workspace(M, p.N, p.K, prec, dev, gemm_only=True))
+        self.W, self.C, self.sid = [], [], []
+        for l in range(nlayers):
+            Ws, sids = [], []
+            for p in self.projs:
+                W = torch.randn((p.N, p.K), generator=g, device=dev) * 0.02
+                Ws.append(W.to(torch.bfloat16) if wt == sp.SPLITEE_BF16 else W)
+                sids.append(WL.stream_id(l, p.group))
+            self.W.append(Ws)
+            self.sid.append(sids)
+        torch.cuda.synchronize()
+        # offline corrections (binary32-accurate mode) for the rows the steps consume;
+        # decode keeps them in a 2048-position bank and reads rows [t, t+M)
+        cprec = sp.SPLITEE_PREC_F32 if wt == sp.SPLITEE_F32 else sp.SPLITEE_PREC_BF16X3
+        t0 = time.perf_counter()
+        for l in range(nlayers):
+            Cs = []
+            for i, p in enumerate(self.projs):
+                c = sp.correction(self.W[l][i], M, mech, delta, eps, 0, self.sid[l][i], self.row0, cprec)
+                if bank_rows:
+                    bank = torch.zeros((bank_rows, p.N), dtype=torch.float32, device=dev)
+                    bank[self.row0:self.row0 + M].copy_(c)
+                    c = bank[self.row0:self.row0 + M]
+                Cs.append(c)
+            self.C.append(Cs)
+        torch.cuda.synchronize()
+        self.correction_ms = (time.perf_counter() - t0) * 1e3 / nlayers * self.layers_per_step
+
+    def launches(self, s, events=None):
+        """All kernels of step s (noise + mask, then GEMM + unmask, per projection)."""
+        sp, M = self.sp, self.M
+        base = (s % self.nsets) * self.layers_per_step
+        nproj = len(self.projs)
+        for l in range(base, base + self.layers_per_step):
+            for i, p in enumerate(self.projs):
+                X, Xt, Y = self.X[i], self.Xt[i], self.Y[i]
+                sp.splitee_noise_mask(X, p.K, Xt, self.prec, p.K, M, p.K, self.mech, self.delta,
+                                      self.eps, 0, self.sid[l][i], self.row0)
+                e = 2 * ((l - base) * nproj + i)
+                if events is not None:
+                    events[e].record()
+                W, C = self.W[l][i], self.C[l][i]
+                sp.splitee_masked_linear_unmask(Xt, self.prec, p.K, W, self.wt, p.K, C, C.stride(0), Y,
+                                                p.N, M, p.N, p.K, self.ws[i][0], self.ws[i][1])
+                if events is not None:
+                    events[e + 1].record()
+
+    def flops(self):
+        return self.layers_per_step * sum(2.0 * self.M * p.N * p.K for p in self.projs)
+
+    def gemm_bytes(self):
+        """Algorithmic bytes of each GEMM + unmask launch: W, float32 X, C and Y."""
+        wb = 4.0 if self.w_dtype == "f32" else 2.0
+        return [wb * p.N * p.K + 4.0 * self.M * p.K + 8.0 * self.M * p.N for p in self.projs]
+
+
+def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
+    path = Path(torch, sp, WL, name, prec, sp.MECHS[args.mech], args.delta, args.eps,
+                args.weight_sets)
+    nsets = path.nsets
+    graphs = None
+    if not args.no_graph:
+        # one HIP graph per step variant; capturing records the same kernels
+        for s in range(nsets):
+            path.launches(s)  # warm the launch path before capture
+        torch.cuda.synchronize()
+        graphs = []
+        for s in range(nsets):
+            gph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gph):
+                path.launches(s)
+            graphs.append(gph)
+        torch.cuda.synchronize()
+
+    def run(s):
+        if graphs is not None:
+            graphs[s % nsets].replay()
+        else:
+            path.launches(s)
+
+    for s in range(warmup):
+        run(s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        run(s)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+
+    # per-launch durations of the GEMM + unmask kernel: HIP events recorded on the
+    # stream the kernels run on, around every launch of an eager pass of as many
+    # steps; averaged per projection group over steps and layers
+    nproj, L = len(path.projs), path.layers_per_step
+    per_proj_us = [0.0] * nproj
+    evs = []
+    torch.cuda.synchronize()
+    for s in range(steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * nproj * L)]
+        path.launches(s, e)
+        evs.append(e)
+    torch.cuda.synchronize()
+    for e in evs:
+        for l in range(L):
+            for i in range(nproj):
+                k = 2 * (l * nproj + i)
+                per_proj_us[i] += e[k].elapsed_time(e[k + 1]) * 1e3 / (steps * L)
+    return path, ms, per_proj_us
+
+
+def cpu_baseline(WL, target_s, projs, tokens, w_dtype):
+    """The oracle (binary128 noise, mask, binary64 GEMM, correction GEMM, unmask) on
+    a row sample of one layer of the same workload; throughput in TFLOP/s of the
+    sample's algorithmic work (2 x rows x N x K per projection group)."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    Ws = [WL.gen_w(p.N, p.K, seed=2 + p.group, dtype=w_dtype) for p in projs]
+
+    def run(rows):
+        t0 = time.perf_counter()
+        for p, W in zip(projs, Ws):
+            X = WL.gen_x(rows, p.K, seed=1)
+            sid = WL.stream_id(0, p.group)
+            eta = O.noise(rows, p.K, O.MECH_GAUSSIAN, 1.0, 1.0, 0, sid, 0)
+            Xt = O.mask(X, eta)
+            R = O.gemm64(Xt, W).astype(np.float32)
+            C = O.gemm64(eta, W).astype(np.float32)
+            O.unmask(R, C)
+        return time.perf_counter() - t0
+
+    run(1)
+    t1 = run(2)
+    rows = int(max(1, min(tokens, 2 * target_s / max(t1, 1e-3))))
+    t = run(rows)
+    flops = sum(2.0 * rows * p.N * p.K for p in projs)
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s",
+            "cores": int(max(O.num_threads(), blas_threads)), "kind": "oracle",
+            "sample": "%d of %d tokens of one layer's %d projection group(s): noise, mask, GEMM, "
+                      "correction GEMM, unmask; %.1f s" % (rows, tokens, len(projs), t)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the masked linear layer runs on a single MI355X "
+              "(multi-GPU sharding is a design note, not part of this build); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_15039_amd as sp
+    import workloads as WL
+    sp.load()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    prec = sp.PRECS[args.prec]
+    if args.workload == "single-fp32-m32":
+        prec = sp.SPLITEE_PREC_F32
+    path, ms, per_proj_us = run_mode(torch, sp, WL, args.workload, prec, args, args.steps, args.warmup)
+    flops = path.flops()
+    value = flops / (ms * 1e-3) / 1e12
+    gb = path.gemm_bytes()
+    gemm_us = sum(per_proj_us)
+    gflops = [2.0 * path.M * p.N * p.K for p in path.projs]
+    ai = sum(gflops) / sum(gb)
+    if ai < 315.0 or path.w_dtype == "f32" and ai < 19.7:
+        achieved = sum(gb) / (gemm_us * 1e-6) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        peak = FP32_PEAK_TFS if prec == sp.SPLITEE_PREC_F32 else BF16_PEAK_TFS
+        achieved = sum(gflops) / (gemm_us * 1e-6) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                    "frac": round(achieved / peak, 4)}
+    roofline.update({"traffic": None, "kernel": "GEMM + unmask (one launch per projection group)",
+                     "launch_us": {p.name: round(u, 2) for p, u in zip(path.projs, per_proj_us)},
+                     "bytes_per_launch": {p.name: int(b) for p, b in zip(path.projs, gb)},
+                     "flops_per_launch": {p.name: int(f) for p, f in zip(path.projs, gflops)},
+                     "algorithmic_ai": round(ai, 1)})
+    modes = {}
+    if not args.no_modes and args.workload != "single-fp32-m32":
+        for mname in ("bf16x3", "bf16", "f32"):
+            if sp.PRECS[mname] == prec:
+                continue
+            _, m_ms, m_pp = run_mode(torch, sp, WL, args.workload, sp.PRECS[mname], args,
+                                     max(10, args.steps // 2), 3)
+            modes[mname] = {"ms_per_step": round(m_ms, 4),
+                            "tflops": round(flops / (m_ms * 1e-3) / 1e12, 2),
+                            "gemm_us": {p.name: round(u, 2) for p, u in zip(path.projs, m_pp)}}
+    pname = {v: k for k, v in sp.PRECS.items()}[prec]
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": pname,
+        "data": "synthetic (seeded random activations and random-init weights)",
+        "config": {"workload": args.workload, "tokens": path.M, "layers_per_step": path.layers_per_step,
+                   "projections": {p.name: [p.K, p.N] for p in path.projs},
+                   "mechanism": args.mech, "delta": args.delta, "eps": args.eps,
+                   "precision": pname, "weight_sets": path.nsets, "row0": path.row0,
+                   "launch": "eager" if args.no_graph else "hip-graph"},
+        "roofline": roofline,
+        "correction_ms": round(path.correction_ms, 4),
+        "modes": modes,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(WL, args.cpu_seconds, path.projs, path.M, path.w_dtype)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

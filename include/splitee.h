@@ -1,0 +1,220 @@
+/*
+ * splitee.h -- C ABI of the MI355X (gfx950) DP-masked linear layer.
+ *
+ * The method (SpliTEE, Sec. "Offloading Linear Operations", Eq.
+ * add-and-then-subtract): to offload y = W x, the trusted side draws a mask eta,
+ * sends x + eta, the GPU returns r = W (x + eta), and the trusted side recovers
+ * W x = r - W eta with the correction W eta computed in advance (Sec.
+ * "Precomputing the Mask and Noise Correction").  The mask is differentially
+ * private noise of scale Delta/eps (Prop. 2; Sec. "Making the Process
+ * Differentially Private"); Delta is the global l2-sensitivity of the function
+ * producing x (Def. 2, Thms 1-3).
+ *
+ * Row-major conventions for every entry point (all sizes in elements):
+ *   X    M x K float32, leading dimension ldx  -- tokens x in-features
+ *   eta  M x K float32 (same shape as X)
+ *   W    N x K, float32 or bfloat16, ldw       -- out x in (the paper's d' x d
+ *                                                 matrix acting on column vectors)
+ *   R, C, Y  M x N float32                     -- Y = X W^T
+ *
+ * Ownership: every pointer is a device pointer owned by the caller; the library
+ * allocates no device memory.  Scratch space is passed in as `workspace`, sized by
+ * the matching *_workspace_bytes query.
+ *
+ * Asynchrony: work is enqueued on `stream` (a hipStream_t; NULL = the default
+ * stream) and the call returns after the launch.  SPLITEE_ERR_HIP reports a
+ * failed launch; faults during execution surface at the caller's synchronize.
+ *
+ * Validation (synchronous; nothing is launched on error):
+ *   eps finite and > 0, Delta finite and >= 0, mechanism known  -> SPLITEE_ERR_ARG
+ *   M, N, K >= 0, ld >= row width, K % 4 == 0 (noise, mask) or
+ *   K % 8 == 0 (GEMM entry points)                                -> SPLITEE_ERR_SHAPE
+ *   16-byte aligned base pointers and 16-byte row pitches        -> SPLITEE_ERR_ALIGN
+ *   unsupported dtype / precision pair                            -> SPLITEE_ERR_UNSUPPORTED
+ *   null pointer where data is required                           -> SPLITEE_ERR_ARG
+ *   workspace too small                                           -> SPLITEE_ERR_WORKSPACE
+ * M == 0 or N == 0 is a valid empty call that launches nothing.
+ *
+ * Noise stream (the paper fixes the law but names no generator; this is the
+ * library's definition, a pure function of its arguments, with no hidden state):
+ *   element (i, k), absolute index e = (row0 + i) K + k, block b = e / 4,
+ *   lane = e % 4; (w0..w3) = Philox4x32-10(counter = (b_lo, b_hi, sid_lo, sid_hi),
+ *   key = (seed_lo, seed_hi)) [Salmon et al., SC'11]; u(w) = (w + 1/2) 2^-32;
+ *   s = fl64(Delta / eps);
+ *   LAPLACE:  eta = RN32(fl64(s * RN32(F^-1(u(w_lane))))), F^-1(u) = ln 2u (u < 1/2),
+ *             -ln(2 - 2u) (u >= 1/2);
+ *   GAUSSIAN: pairs (w0,w1) -> lanes 0,1 and (w2,w3) -> lanes 2,3 (Box-Muller):
+ *             r = RN32(sqrt(-2 ln u(w_a))), c = RN32(cos 2 pi u(w_b)), sn = RN32(sin 2 pi u(w_b)),
+ *             eta = RN32(fl64(s * (r * c))) on even lanes, RN32(fl64(s * (r * sn))) on odd;
+ *   NONE:     eta = 0 (the split without noise).
+ * RN32 is the correctly rounded binary32 value.  Single use of a mask
+ * (Sec. "Precomputing the Mask and Noise Correction") is the caller's duty: never
+ * reissue the same (seed, stream_id, row).
+ *
+ * Precision modes of the GEMM operand built from Xt = fl32(X + eta):
+ *   SPLITEE_PREC_F32    Xt as float32, binary32 MFMA (bfloat16 W widened exactly).
+ *   SPLITEE_PREC_BF16   Xt rounded once to bfloat16 (single pass; adds u_bf16 * sum|w||Xt|).
+ *   SPLITEE_PREC_BF16X3 Xt = hi + mid + lo as three bfloat16 terms (exact), three
+ *                       bfloat16 MFMA passes into one float32 accumulator; needs bf16 W.
+ * BF16 and BF16X3 planes are stored one after another, plane p at
+ * Xt + p * M * ldxt elements.
+ *
+ * Thread safety: the functions are stateless and reentrant.  Calls that share a
+ * workspace must not overlap in time.
+ *
+ * Trust note: the fused call and splitee_correction place eta on the GPU.  That is
+ * the one-GPU benchmark arrangement; in the paper's deployment only the GEMM of
+ * the masked input (splitee_masked_linear) runs on the untrusted device and the
+ * correction is computed inside the TEE.
+ */
+#ifndef SPLITEE_H
+#define SPLITEE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPLITEE_ABI_VERSION 1
+
+typedef enum {
+    SPLITEE_OK = 0,
+    SPLITEE_ERR_ARG = -1,
+    SPLITEE_ERR_SHAPE = -2,
+    SPLITEE_ERR_DTYPE = -3,
+    SPLITEE_ERR_ALIGN = -4,
+    SPLITEE_ERR_UNSUPPORTED = -5,
+    SPLITEE_ERR_HIP = -6,
+    SPLITEE_ERR_WORKSPACE = -7
+} splitee_status;
+
+typedef enum { SPLITEE_MECH_LAPLACE = 0, SPLITEE_MECH_GAUSSIAN = 1, SPLITEE_MECH_NONE = 2 } splitee_mech;
+typedef enum { SPLITEE_F32 = 0, SPLITEE_BF16 = 1 } splitee_dtype;
+typedef enum { SPLITEE_PREC_F32 = 0, SPLITEE_PREC_BF16 = 1, SPLITEE_PREC_BF16X3 = 2 } splitee_prec;
+
+/* Version of this ABI (SPLITEE_ABI_VERSION). */
+int splitee_abi_version(void);
+
+/* Static text for a status code. */
+const char* splitee_status_string(int status);
+
+/*
+ * Noise eta (the mask; Prop. 2, Sec. "Making the Process Differentially Private").
+ *   eta       out, M x K float32, leading dimension ld_eta (>= K, multiple of 4)
+ *   mech      splitee_mech; sensitivity = Delta >= 0; epsilon > 0
+ *   seed, stream_id, row0   select the counter block (see "Noise stream" above)
+ * Requires K % 4 == 0.
+ */
+int splitee_noise_gen(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech,
+                      double sensitivity, double epsilon, uint64_t seed, uint64_t stream_id,
+                      uint64_t row0, void* stream);
+
+/*
+ * Mask: Xt = fl32(X + eta) (the vector addition of Sec. "Offloading Linear
+ * Operations"), written in precision out_prec:
+ *   F32: float32 M x K (ldxt); BF16: one bfloat16 plane; BF16X3: three bfloat16
+ *   planes hi, mid, lo (plane p at Xt + p * M * ldxt).
+ *   X may be NULL, meaning X = 0 (used to split eta for the correction).
+ * Requires K % 4 == 0; ldxt a multiple of 8 for bfloat16 output, of 4 for float32.
+ */
+int splitee_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, void* Xt,
+                 int out_prec, int64_t ldxt, int64_t M, int64_t K, void* stream);
+
+/*
+ * Noise and mask in one pass: Xt = fl32(X + eta) with eta generated in-kernel from
+ * (mech, Delta, eps, seed, stream_id, row0) exactly as splitee_noise_gen would
+ * produce it; eta itself is never stored.  Output layout as in splitee_mask.
+ * X may be NULL (Xt = eta, as needed for the correction).  Requires K % 4 == 0.
+ * This is the first half of splitee_masked_linear_fused.
+ */
+int splitee_noise_mask(const float* X, int64_t ldx, void* Xt, int out_prec, int64_t ldxt, int64_t M,
+                       int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                       uint64_t stream_id, uint64_t row0, void* stream);
+
+/*
+ * The GPU's part of the method: R = Xt W^T (r = W (x + eta), Sec. "Offloading
+ * Linear Operations"), with float32 accumulation.
+ *   Xt     in_prec operand as written by splitee_mask (ldxt)
+ *   W      N x K, w_type float32 or bfloat16 (ldw); BF16 / BF16X3 need bfloat16 W
+ *   R      out, M x N float32 (ldr)
+ * Requires K % 8 == 0.  Needs no workspace (single-pass K reduction per tile).
+ */
+int splitee_masked_linear(const void* Xt, int in_prec, int64_t ldxt, const void* W, int w_type,
+                          int64_t ldw, float* R, int64_t ldr, int64_t M, int64_t N, int64_t K,
+                          void* stream);
+
+/*
+ * Unmask: Y = fl32(R - C) (Eq. add-and-then-subtract), C the correction eta W^T.
+ * Requires 16-byte aligned rows.
+ */
+int splitee_unmask(const float* R, int64_t ldr, const float* C, int64_t ldc, float* Y, int64_t ldy,
+                   int64_t M, int64_t N, void* stream);
+
+/* Workspace bytes needed by splitee_masked_linear_unmask for this shape and
+ * precision (split-K counters and partial tiles); 0 when none is needed. */
+size_t splitee_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
+
+/*
+ * GEMM with the unmask epilogue: Y = fl32(fl(Xt W^T) - C) (C NULL: Y = R), the
+ * second half of splitee_masked_linear_fused.  Xt as written by splitee_mask or
+ * splitee_noise_mask (ldxt, planes M * ldxt apart).  Small tile counts are split
+ * over K; the partial tiles are summed in a fixed order by the last workgroup of
+ * each tile, so results are deterministic.  workspace: >=
+ * splitee_gemm_workspace_bytes bytes, 256-byte aligned, zero-filled before its
+ * first use (calls leave it zeroed).  Requires K % 8 == 0.
+ */
+int splitee_masked_linear_unmask(const void* Xt, int in_prec, int64_t ldxt, const void* W,
+                                 int w_type, int64_t ldw, const float* C, int64_t ldc, float* Y,
+                                 int64_t ldy, int64_t M, int64_t N, int64_t K, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by splitee_masked_linear_fused (and splitee_correction)
+ * for this shape and precision; 0 on invalid arguments. */
+size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
+
+/*
+ * Fused mask -> GEMM -> unmask for one projection: Y = fl32(fl(Xt W^T) - C) with
+ * Xt = fl32(X + eta), eta generated in-stream from (mech, Delta, eps, seed,
+ * stream_id, row0) -- or taken from eta_override when it is not NULL (M x K float32,
+ * leading dimension K; tests inject integer masks this way).  C (M x N, ldc) must be the correction of the same
+ * mask, e.g. from splitee_correction with the same noise arguments; for a decode
+ * step at positions [t, t+M) pass row0 = t and C = bank + t * ldc.
+ * M <= 16 with BF16 or BF16X3 takes the skinny bandwidth-bound kernel (decode);
+ * otherwise the tiled MFMA kernel runs, split over K when the tile count is small.  workspace: >= splitee_fused_workspace_bytes(M, N, K, prec)
+ * bytes, 256-byte aligned; it must hold zeros before its first use and calls
+ * leave it that way.
+ */
+int splitee_masked_linear_fused(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
+                                const float* C, int64_t ldc, float* Y, int64_t ldy, int64_t M,
+                                int64_t N, int64_t K, int mech, double sensitivity, double epsilon,
+                                uint64_t seed, uint64_t stream_id, uint64_t row0,
+                                const float* eta_override, int prec, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/*
+ * Correction C = eta W^T (Sec. "Precomputing the Mask and Noise Correction"),
+ * computed in F32 or BF16X3 (single-pass BF16 would round eta and break the
+ * cancellation: SPLITEE_ERR_UNSUPPORTED).  Noise arguments as in the fused call.
+ * In the paper this runs offline inside the TEE.
+ */
+int splitee_correction(float* C, int64_t ldc, const void* W, int w_type, int64_t ldw, int64_t M,
+                       int64_t N, int64_t K, int mech, double sensitivity, double epsilon,
+                       uint64_t seed, uint64_t stream_id, uint64_t row0, int prec, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * Test hook: evaluates one correctly rounded noise transform on n words
+ * (fn 0: Laplace inverse CDF, 1: sqrt(-2 ln u), 2: cos 2 pi u, 3: sin 2 pi u).
+ * force_slow = 1 takes the double-double path for every word instead of only
+ * for words whose binary64 value lies near a binary32 rounding boundary.
+ */
+int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_slow, float* out,
+                            void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPLITEE_H */

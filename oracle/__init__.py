@@ -58,12 +58,19 @@ def _load():
     lib.oracle_noise.argtypes = [P, i64, i64, i64, ctypes.c_int, ctypes.c_double,
                                  ctypes.c_double, u64, u64, u64]
     lib.oracle_noise.restype = ctypes.c_int
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
 
 
 def _ptr(a):
     return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def num_threads():
+    """OpenMP threads of the oracle's C part."""
+    return _load().oracle_num_threads()
 
 
 # --------------------------------------------------------------------------- noise

@@ -37,6 +37,7 @@
  * status code instead of being returned silently.
  */
 #include <math.h>
+#include <omp.h>
 #include <quadmath.h>
 #include <stdint.h>
 #include <string.h>
@@ -45,6 +46,9 @@
 #define ORC_ERR_SHAPE (-2)
 #define ORC_ERR_ARG (-1)
 #define ORC_ERR_HARD_ROUNDING (-7)
+
+/* Number of OpenMP threads the oracle runs on. */
+int oracle_num_threads(void) { return omp_get_max_threads(); }
 
 /* ---- Philox4x32-10 -------------------------------------------------------- */
 

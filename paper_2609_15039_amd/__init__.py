@@ -1,0 +1,271 @@
+"""Python binding of libsplitee.so, the MI355X DP-masked linear layer.
+
+Argument marshalling only: every function below forwards to the C entry point
+of the same name (declared in include/splitee.h) with device pointers taken
+from torch tensors and the current torch stream.  All arithmetic runs in the
+HIP kernels; there is no fallback.  If the library is not built the import
+still works but every call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsplitee.so")
+
+SPLITEE_OK = 0
+SPLITEE_MECH_LAPLACE, SPLITEE_MECH_GAUSSIAN, SPLITEE_MECH_NONE = 0, 1, 2
+SPLITEE_F32, SPLITEE_BF16 = 0, 1
+SPLITEE_PREC_F32, SPLITEE_PREC_BF16, SPLITEE_PREC_BF16X3 = 0, 1, 2
+MECHS = {"laplace": SPLITEE_MECH_LAPLACE, "gaussian": SPLITEE_MECH_GAUSSIAN, "none": SPLITEE_MECH_NONE}
+PRECS = {"f32": SPLITEE_PREC_F32, "bf16": SPLITEE_PREC_BF16, "bf16x3": SPLITEE_PREC_BF16X3}
+
+EXPORTED = [
+    "splitee_abi_version", "splitee_status_string", "splitee_noise_gen", "splitee_mask",
+    "splitee_masked_linear", "splitee_unmask", "splitee_fused_workspace_bytes",
+    "splitee_masked_linear_fused", "splitee_correction", "splitee_transform_probe",
+    "splitee_noise_mask", "splitee_gemm_workspace_bytes", "splitee_masked_linear_unmask",
+]
+
+
+class SpliteeError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (fn, _status_text(status), status))
+
+
+_lib = None
+
+
+def load():
+    """Load libsplitee.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libsplitee.so is not built (run __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I, I64, U64, D, SZ = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64,
+                             ctypes.c_double, ctypes.c_size_t)
+    sig = {
+        "splitee_abi_version": (I, []),
+        "splitee_status_string": (ctypes.c_char_p, [I]),
+        "splitee_noise_gen": (I, [P, I64, I64, I64, I, D, D, U64, U64, U64, P]),
+        "splitee_mask": (I, [P, I64, P, I64, P, I, I64, I64, I64, P]),
+        "splitee_masked_linear": (I, [P, I, I64, P, I, I64, P, I64, I64, I64, I64, P]),
+        "splitee_unmask": (I, [P, I64, P, I64, P, I64, I64, I64, P]),
+        "splitee_fused_workspace_bytes": (SZ, [I64, I64, I64, I]),
+        "splitee_masked_linear_fused": (I, [P, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, I, D, D,
+                                            U64, U64, U64, P, I, P, SZ, P]),
+        "splitee_correction": (I, [P, I64, P, I, I64, I64, I64, I64, I, D, D, U64, U64, U64, I, P, SZ,
+                                   P]),
+        "splitee_transform_probe": (I, [P, I64, I, I, P, P]),
+        "splitee_noise_mask": (I, [P, I64, P, I, I64, I64, I64, I, D, D, U64, U64, U64, P]),
+        "splitee_gemm_workspace_bytes": (SZ, [I64, I64, I64, I]),
+        "splitee_masked_linear_unmask": (I, [P, I, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, P,
+                                             SZ, P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _status_text(status):
+    try:
+        return load().splitee_status_string(status).decode()
+    except Exception:  # library missing
+        return "status"
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return stream
+
+
+def _check(fn, status):
+    if status != SPLITEE_OK:
+        raise SpliteeError(fn, status)
+
+
+def _wtype(W):
+    return SPLITEE_BF16 if W.dtype == torch.bfloat16 else SPLITEE_F32
+
+
+# ------------------------------------------------------------ C entry points
+
+def splitee_abi_version():
+    return load().splitee_abi_version()
+
+
+def splitee_status_string(status):
+    return load().splitee_status_string(status).decode()
+
+
+def splitee_noise_gen(eta, ld_eta, M, K, mech, sensitivity, epsilon, seed, stream_id, row0=0,
+                      stream=None):
+    _check("splitee_noise_gen", load().splitee_noise_gen(
+        _ptr(eta), ld_eta, M, K, mech, sensitivity, epsilon, seed, stream_id, row0, _stream(stream)))
+
+
+def splitee_mask(X, ldx, eta, ld_eta, Xt, out_prec, ldxt, M, K, stream=None):
+    _check("splitee_mask", load().splitee_mask(
+        _ptr(X), ldx, _ptr(eta), ld_eta, _ptr(Xt), out_prec, ldxt, M, K, _stream(stream)))
+
+
+def splitee_masked_linear(Xt, in_prec, ldxt, W, w_type, ldw, R, ldr, M, N, K, stream=None):
+    _check("splitee_masked_linear", load().splitee_masked_linear(
+        _ptr(Xt), in_prec, ldxt, _ptr(W), w_type, ldw, _ptr(R), ldr, M, N, K, _stream(stream)))
+
+
+def splitee_unmask(R, ldr, C, ldc, Y, ldy, M, N, stream=None):
+    _check("splitee_unmask", load().splitee_unmask(
+        _ptr(R), ldr, _ptr(C), ldc, _ptr(Y), ldy, M, N, _stream(stream)))
+
+
+def splitee_fused_workspace_bytes(M, N, K, prec):
+    return load().splitee_fused_workspace_bytes(M, N, K, prec)
+
+
+def splitee_masked_linear_fused(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, mech, sensitivity,
+                                epsilon, seed, stream_id, row0, eta_override, prec, workspace,
+                                workspace_bytes, stream=None):
+    _check("splitee_masked_linear_fused", load().splitee_masked_linear_fused(
+        _ptr(X), ldx, _ptr(W), w_type, ldw, _ptr(C), ldc, _ptr(Y), ldy, M, N, K, mech, sensitivity,
+        epsilon, seed, stream_id, row0, _ptr(eta_override), prec, _ptr(workspace), workspace_bytes,
+        _stream(stream)))
+
+
+def splitee_correction(C, ldc, W, w_type, ldw, M, N, K, mech, sensitivity, epsilon, seed,
+                       stream_id, row0, prec, workspace, workspace_bytes, stream=None):
+    _check("splitee_correction", load().splitee_correction(
+        _ptr(C), ldc, _ptr(W), w_type, ldw, M, N, K, mech, sensitivity, epsilon, seed, stream_id,
+        row0, prec, _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def splitee_transform_probe(words, n, fn, force_slow, out, stream=None):
+    _check("splitee_transform_probe", load().splitee_transform_probe(
+        _ptr(words), n, fn, force_slow, _ptr(out), _stream(stream)))
+
+
+def splitee_noise_mask(X, ldx, Xt, out_prec, ldxt, M, K, mech, sensitivity, epsilon, seed,
+                       stream_id, row0=0, stream=None):
+    _check("splitee_noise_mask", load().splitee_noise_mask(
+        _ptr(X), ldx, _ptr(Xt), out_prec, ldxt, M, K, mech, sensitivity, epsilon, seed, stream_id,
+        row0, _stream(stream)))
+
+
+def splitee_gemm_workspace_bytes(M, N, K, prec):
+    return load().splitee_gemm_workspace_bytes(M, N, K, prec)
+
+
+def splitee_masked_linear_unmask(Xt, in_prec, ldxt, W, w_type, ldw, C, ldc, Y, ldy, M, N, K,
+                                 workspace, workspace_bytes, stream=None):
+    _check("splitee_masked_linear_unmask", load().splitee_masked_linear_unmask(
+        _ptr(Xt), in_prec, ldxt, _ptr(W), w_type, ldw, _ptr(C), ldc, _ptr(Y), ldy, M, N, K,
+        _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+# ------------------------------------------------- tensor-level conveniences
+
+def workspace(M, N, K, prec, device="cuda", gemm_only=False):
+    """A zeroed, 256-byte aligned workspace for the fused call / correction (or, with
+    gemm_only, for splitee_masked_linear_unmask); returns (tensor, bytes)."""
+    nbytes = (splitee_gemm_workspace_bytes if gemm_only else splitee_fused_workspace_bytes)(M, N, K, prec)
+    ws = torch.zeros(max(nbytes, 1) + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + max(nbytes, 1)], nbytes
+
+
+def noise(M, K, mech, sensitivity, epsilon, seed, stream_id, row0=0, device="cuda"):
+    eta = torch.empty((M, K), dtype=torch.float32, device=device)
+    splitee_noise_gen(eta, K, M, K, mech, sensitivity, epsilon, seed, stream_id, row0)
+    return eta
+
+
+def mask(X, eta, prec):
+    M, K = X.shape
+    planes = 3 if prec == SPLITEE_PREC_BF16X3 else 1
+    dt = torch.float32 if prec == SPLITEE_PREC_F32 else torch.int16
+    Xt = torch.empty((planes, M, K), dtype=dt, device=X.device)
+    splitee_mask(X, X.stride(0), eta, eta.stride(0), Xt, prec, K, M, K)
+    return Xt
+
+
+def masked_linear(Xt, prec, W):
+    M, K = Xt.shape[-2:]
+    N = W.shape[0]
+    R = torch.empty((M, N), dtype=torch.float32, device=W.device)
+    splitee_masked_linear(Xt, prec, K, W, _wtype(W), W.stride(0), R, N, M, N, K)
+    return R
+
+
+def noise_mask(X, prec, mech, sensitivity, epsilon, seed, stream_id, row0=0):
+    M, K = X.shape
+    planes = 3 if prec == SPLITEE_PREC_BF16X3 else 1
+    dt = torch.float32 if prec == SPLITEE_PREC_F32 else torch.int16
+    Xt = torch.empty((planes, M, K), dtype=dt, device=X.device)
+    splitee_noise_mask(X, X.stride(0), Xt, prec, K, M, K, mech, sensitivity, epsilon, seed,
+                       stream_id, row0)
+    return Xt
+
+
+def masked_linear_unmask(Xt, prec, W, C, ws=None, Y=None):
+    M, K = Xt.shape[-2:]
+    N = W.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=W.device)
+    if ws is None:
+        ws = workspace(M, N, K, prec, W.device, gemm_only=True)
+    splitee_masked_linear_unmask(Xt, prec, K, W, _wtype(W), W.stride(0), C,
+                                 C.stride(0) if C is not None else 0, Y, Y.stride(0), M, N, K,
+                                 ws[0], ws[1])
+    return Y
+
+
+def unmask(R, C):
+    M, N = R.shape
+    Y = torch.empty((M, N), dtype=torch.float32, device=R.device)
+    splitee_unmask(R, R.stride(0), C, C.stride(0), Y, N, M, N)
+    return Y
+
+
+def correction(W, M, mech, sensitivity, epsilon, seed, stream_id, row0=0, prec=SPLITEE_PREC_BF16X3,
+               ws=None):
+    N, K = W.shape
+    C = torch.empty((M, N), dtype=torch.float32, device=W.device)
+    if ws is None:
+        ws = workspace(M, N, K, prec, W.device)
+    splitee_correction(C, N, W, _wtype(W), W.stride(0), M, N, K, mech, sensitivity, epsilon, seed,
+                       stream_id, row0, prec, ws[0], ws[1])
+    return C
+
+
+def masked_linear_fused(X, W, C, mech, sensitivity, epsilon, seed, stream_id, row0=0,
+                        prec=SPLITEE_PREC_BF16X3, eta_override=None, ws=None, Y=None):
+    M, K = X.shape
+    N = W.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = workspace(M, N, K, prec, X.device)
+    splitee_masked_linear_fused(X, X.stride(0), W, _wtype(W), W.stride(0), C, C.stride(0), Y,
+                                Y.stride(0), M, N, K, mech, sensitivity, epsilon, seed, stream_id,
+                                row0, eta_override, prec, ws[0], ws[1])
+    return Y

@@ -1,0 +1,291 @@
+// C ABI of the DP-masked linear layer: argument validation and kernel launches.
+// Semantics of every entry point are documented in include/splitee.h.
+#include <math.h>
+
+#include "common.hpp"
+
+namespace splitee_host {
+size_t gemm_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);
+size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K);
+}
+
+namespace {
+
+constexpr int64_t MAX_DIM = int64_t(1) << 30;
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+inline bool pitch16(int64_t ld, int64_t elsize) { return (ld * elsize) % 16 == 0; }
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline bool valid_mech(int mech)
+{
+    return mech == SPLITEE_MECH_LAPLACE || mech == SPLITEE_MECH_GAUSSIAN || mech == SPLITEE_MECH_NONE;
+}
+
+inline int check_noise_args(int mech, double sensitivity, double epsilon)
+{
+    if (!valid_mech(mech)) return SPLITEE_ERR_ARG;
+    if (!(epsilon > 0.0) || !isfinite(epsilon)) return SPLITEE_ERR_ARG;
+    if (!(sensitivity >= 0.0) || !isfinite(sensitivity)) return SPLITEE_ERR_ARG;
+    return SPLITEE_OK;
+}
+
+inline bool dims_ok(int64_t M, int64_t N, int64_t K)
+{
+    return M >= 0 && N >= 0 && K >= 0 && M <= MAX_DIM && N <= MAX_DIM && K <= MAX_DIM;
+}
+
+inline int64_t prec_elsize(int prec) { return prec == SPLITEE_PREC_F32 ? 4 : 2; }
+inline int64_t prec_planes(int prec) { return prec == SPLITEE_PREC_BF16X3 ? 3 : 1; }
+inline bool valid_prec(int prec)
+{
+    return prec == SPLITEE_PREC_F32 || prec == SPLITEE_PREC_BF16 || prec == SPLITEE_PREC_BF16X3;
+}
+inline bool valid_dtype(int t) { return t == SPLITEE_F32 || t == SPLITEE_BF16; }
+
+// Skinny kernel for decode-sized M with bfloat16 operands, tiled kernel otherwise.
+inline bool use_skinny(int64_t M, int prec) { return M <= 16 && prec != SPLITEE_PREC_F32; }
+
+size_t gemm_ws(int64_t M, int64_t N, int64_t K, int prec, int w_type)
+{
+    return use_skinny(M, prec) ? splitee_host::skinny_workspace_bytes(M, N, K, prec)
+                               : splitee_host::gemm_workspace_bytes(M, N, K, prec, w_type);
+}
+size_t gemm_counters(int64_t M, int64_t N, int64_t K, int prec, int w_type)
+{
+    return use_skinny(M, prec) ? splitee_host::skinny_counter_bytes(M, N, K)
+                               : splitee_host::gemm_counter_bytes(M, N, K, prec, w_type);
+}
+
+// GEMM operand checks shared by the GEMM entry points.
+int check_w(const void* W, int w_type, int64_t ldw, int64_t K, int prec)
+{
+    if (!valid_dtype(w_type)) return SPLITEE_ERR_DTYPE;
+    if (prec != SPLITEE_PREC_F32 && w_type != SPLITEE_BF16) return SPLITEE_ERR_UNSUPPORTED;
+    const int64_t wes = w_type == SPLITEE_F32 ? 4 : 2;
+    if (ldw < K) return SPLITEE_ERR_SHAPE;
+    if (!aligned16(W) || !pitch16(ldw, wes)) return SPLITEE_ERR_ALIGN;
+    return SPLITEE_OK;
+}
+
+// GEMM (+ unmask) on a masked input already in memory.
+int run_gemm(const void* Xt, int prec, int64_t ldxt, const void* W, int w_type, int64_t ldw,
+             const float* C, int64_t ldc, float* Y, int64_t ldy, int64_t M, int64_t N, int64_t K,
+             void* ws, size_t ws_bytes, hipStream_t s)
+{
+    if (use_skinny(M, prec))
+        return splitee_host::launch_skinny(Xt, prec, ldxt, M * ldxt, W, ldw, C, ldc, Y, ldy, M, N, K, ws,
+                                           ws_bytes, s);
+    return splitee_host::launch_gemm(Xt, prec, ldxt, M * ldxt, W, w_type, ldw, C, ldc, Y, ldy, M, N, K,
+                                     ws, ws_bytes, s);
+}
+
+// Noise + mask into the workspace, then the GEMM with the unmask epilogue.
+// X == nullptr computes the correction (A = eta, no C).
+int run_masked(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw, const float* C,
+               int64_t ldc, float* Y, int64_t ldy, int64_t M, int64_t N, int64_t K, int mech,
+               double sensitivity, double epsilon, uint64_t seed, uint64_t sid, uint64_t row0,
+               const float* eta_override, int prec, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    const size_t gws = align256(gemm_ws(M, N, K, prec, w_type));
+    const size_t need = gws + align256((size_t)(prec_planes(prec) * M * K * prec_elsize(prec)));
+    if (ws_bytes < need || (need > 0 && ws == nullptr)) return SPLITEE_ERR_WORKSPACE;
+    if (ws && (reinterpret_cast<uintptr_t>(ws) & 255u)) return SPLITEE_ERR_ALIGN;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    char* base = reinterpret_cast<char*>(ws);
+    void* Xt = base + gws;
+    unsigned* counters = reinterpret_cast<unsigned*>(base);
+    const int64_t ncounters = (int64_t)(gemm_counters(M, N, K, prec, w_type) / 4);
+    const double scale = sensitivity / epsilon;
+    int rc = splitee_host::launch_mask(X, ldx, eta_override, K, mech, scale, seed, sid, row0, Xt, prec,
+                                       K, M * K, M, K, counters, ncounters, s);
+    if (rc != SPLITEE_OK) return rc;
+    return run_gemm(Xt, prec, K, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, base, gws, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int splitee_abi_version(void) { return SPLITEE_ABI_VERSION; }
+
+const char* splitee_status_string(int status)
+{
+    switch (status) {
+    case SPLITEE_OK: return "ok";
+    case SPLITEE_ERR_ARG: return "invalid argument (mechanism, sensitivity, epsilon or null pointer)";
+    case SPLITEE_ERR_SHAPE: return "invalid shape or leading dimension";
+    case SPLITEE_ERR_DTYPE: return "invalid data type";
+    case SPLITEE_ERR_ALIGN: return "pointer or row pitch not 16-byte aligned";
+    case SPLITEE_ERR_UNSUPPORTED: return "unsupported precision / data type combination";
+    case SPLITEE_ERR_HIP: return "HIP launch failed";
+    case SPLITEE_ERR_WORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+    }
+}
+
+int splitee_noise_gen(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech,
+                      double sensitivity, double epsilon, uint64_t seed, uint64_t stream_id,
+                      uint64_t row0, void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (!dims_ok(M, 0, K) || K % 4 != 0 || ld_eta < K) return SPLITEE_ERR_SHAPE;
+    if (M == 0 || K == 0) return SPLITEE_OK;
+    if (!eta) return SPLITEE_ERR_ARG;
+    if (!aligned16(eta) || !pitch16(ld_eta, 4)) return SPLITEE_ERR_ALIGN;
+    return splitee_host::launch_noise(eta, ld_eta, M, K, mech, sensitivity / epsilon, seed, stream_id,
+                                      row0, as_stream(stream));
+}
+
+int splitee_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, void* Xt,
+                 int out_prec, int64_t ldxt, int64_t M, int64_t K, void* stream)
+{
+    if (!valid_prec(out_prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, 0, K) || K % 4 != 0 || ld_eta < K || ldxt < K || (X && ldx < K))
+        return SPLITEE_ERR_SHAPE;
+    if (M == 0 || K == 0) return SPLITEE_OK;
+    if (!eta || !Xt) return SPLITEE_ERR_ARG;
+    if (!aligned16(eta) || !pitch16(ld_eta, 4) || !aligned16(Xt) ||
+        !pitch16(ldxt, prec_elsize(out_prec)) || (X && (!aligned16(X) || !pitch16(ldx, 4))))
+        return SPLITEE_ERR_ALIGN;
+    // bfloat16 rows are written 4 elements (8 bytes) at a time; the 16-byte row
+    // pitch keeps every store aligned.
+    return splitee_host::launch_mask(X, ldx, eta, ld_eta, SPLITEE_MECH_NONE, 0.0, 0, 0, 0, Xt, out_prec,
+                                     ldxt, M * ldxt, M, K, nullptr, 0, as_stream(stream));
+}
+
+int splitee_noise_mask(const float* X, int64_t ldx, void* Xt, int out_prec, int64_t ldxt, int64_t M,
+                       int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                       uint64_t stream_id, uint64_t row0, void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (!valid_prec(out_prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, 0, K) || K % 4 != 0 || ldxt < K || (X && ldx < K)) return SPLITEE_ERR_SHAPE;
+    if (M == 0 || K == 0) return SPLITEE_OK;
+    if (!Xt) return SPLITEE_ERR_ARG;
+    if (!aligned16(Xt) || !pitch16(ldxt, prec_elsize(out_prec)) || (X && (!aligned16(X) || !pitch16(ldx, 4))))
+        return SPLITEE_ERR_ALIGN;
+    return splitee_host::launch_mask(X, ldx, nullptr, 0, mech, sensitivity / epsilon, seed, stream_id,
+                                     row0, Xt, out_prec, ldxt, M * ldxt, M, K, nullptr, 0,
+                                     as_stream(stream));
+}
+
+int splitee_masked_linear(const void* Xt, int in_prec, int64_t ldxt, const void* W, int w_type,
+                          int64_t ldw, float* R, int64_t ldr, int64_t M, int64_t N, int64_t K,
+                          void* stream)
+{
+    if (!valid_prec(in_prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldxt < K || ldr < N) return SPLITEE_ERR_SHAPE;
+    int rc = check_w(W, w_type, ldw, K, in_prec);
+    if (rc) return rc;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!Xt || !W || !R) return SPLITEE_ERR_ARG;
+    if (!aligned16(Xt) || !pitch16(ldxt, prec_elsize(in_prec)) || !aligned16(R) || !pitch16(ldr, 4))
+        return SPLITEE_ERR_ALIGN;
+    return splitee_host::launch_gemm(Xt, in_prec, ldxt, M * ldxt, W, w_type, ldw, nullptr, 0, R, ldr, M,
+                                     N, K, nullptr, 0, as_stream(stream));
+}
+
+int splitee_unmask(const float* R, int64_t ldr, const float* C, int64_t ldc, float* Y, int64_t ldy,
+                   int64_t M, int64_t N, void* stream)
+{
+    if (!dims_ok(M, N, 0) || ldr < N || ldc < N || ldy < N) return SPLITEE_ERR_SHAPE;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!R || !C || !Y) return SPLITEE_ERR_ARG;
+    if (!aligned16(R) || !aligned16(C) || !aligned16(Y) || !pitch16(ldr, 4) || !pitch16(ldc, 4) ||
+        !pitch16(ldy, 4))
+        return SPLITEE_ERR_ALIGN;
+    return splitee_host::launch_unmask(R, ldr, C, ldc, Y, ldy, M, N, as_stream(stream));
+}
+
+size_t splitee_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
+{
+    if (!valid_prec(prec) || !dims_ok(M, N, K) || K % 8 != 0) return 0;
+    return gemm_ws(M, N, K, prec, SPLITEE_BF16);
+}
+
+int splitee_masked_linear_unmask(const void* Xt, int in_prec, int64_t ldxt, const void* W,
+                                 int w_type, int64_t ldw, const float* C, int64_t ldc, float* Y,
+                                 int64_t ldy, int64_t M, int64_t N, int64_t K, void* workspace,
+                                 size_t workspace_bytes, void* stream)
+{
+    if (!valid_prec(in_prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldxt < K || ldy < N || (C && ldc < N)) return SPLITEE_ERR_SHAPE;
+    int rc = check_w(W, w_type, ldw, K, in_prec);
+    if (rc) return rc;
+    const size_t need = gemm_ws(M, N, K, in_prec, w_type);
+    if (workspace_bytes < need || (need > 0 && workspace == nullptr)) return SPLITEE_ERR_WORKSPACE;
+    if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return SPLITEE_ERR_ALIGN;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!Xt || !W || !Y) return SPLITEE_ERR_ARG;
+    if (!aligned16(Xt) || !pitch16(ldxt, prec_elsize(in_prec)) || !aligned16(Y) || !pitch16(ldy, 4) ||
+        (C && (!aligned16(C) || !pitch16(ldc, 4))))
+        return SPLITEE_ERR_ALIGN;
+    return run_gemm(Xt, in_prec, ldxt, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, workspace,
+                    workspace_bytes, as_stream(stream));
+}
+
+size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
+{
+    if (!valid_prec(prec) || !dims_ok(M, N, K) || K % 8 != 0) return 0;
+    const int w_type = SPLITEE_BF16;
+    return align256(gemm_ws(M, N, K, prec, w_type)) +
+           align256((size_t)(prec_planes(prec) * M * K * prec_elsize(prec)));
+}
+
+int splitee_masked_linear_fused(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
+                                const float* C, int64_t ldc, float* Y, int64_t ldy, int64_t M,
+                                int64_t N, int64_t K, int mech, double sensitivity, double epsilon,
+                                uint64_t seed, uint64_t stream_id, uint64_t row0,
+                                const float* eta_override, int prec, void* workspace,
+                                size_t workspace_bytes, void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (!valid_prec(prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldx < K || ldc < N || ldy < N) return SPLITEE_ERR_SHAPE;
+    rc = check_w(W, w_type, ldw, K, prec);
+    if (rc) return rc;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!X || !W || !C || !Y) return SPLITEE_ERR_ARG;
+    if (!aligned16(X) || !pitch16(ldx, 4) || !aligned16(C) || !pitch16(ldc, 4) || !aligned16(Y) ||
+        !pitch16(ldy, 4) || (eta_override && !aligned16(eta_override)))
+        return SPLITEE_ERR_ALIGN;
+    // an injected mask is M x K with leading dimension K
+    return run_masked(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, mech, sensitivity, epsilon,
+                      seed, stream_id, row0, eta_override, prec, workspace, workspace_bytes,
+                      as_stream(stream));
+}
+
+int splitee_correction(float* C, int64_t ldc, const void* W, int w_type, int64_t ldw, int64_t M,
+                       int64_t N, int64_t K, int mech, double sensitivity, double epsilon,
+                       uint64_t seed, uint64_t stream_id, uint64_t row0, int prec, void* workspace,
+                       size_t workspace_bytes, void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (prec == SPLITEE_PREC_BF16 || !valid_prec(prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldc < N) return SPLITEE_ERR_SHAPE;
+    rc = check_w(W, w_type, ldw, K, prec);
+    if (rc) return rc;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!W || !C) return SPLITEE_ERR_ARG;
+    if (!aligned16(C) || !pitch16(ldc, 4)) return SPLITEE_ERR_ALIGN;
+    return run_masked(nullptr, K, W, w_type, ldw, nullptr, 0, C, ldc, M, N, K, mech, sensitivity,
+                      epsilon, seed, stream_id, row0, nullptr, prec, workspace, workspace_bytes,
+                      as_stream(stream));
+}
+
+int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_slow, float* out,
+                            void* stream)
+{
+    if (fn < 0 || fn > 3 || n < 0) return SPLITEE_ERR_ARG;
+    if (n == 0) return SPLITEE_OK;
+    if (!words || !out) return SPLITEE_ERR_ARG;
+    return splitee_host::launch_transform_probe(words, n, fn, force_slow, out, as_stream(stream));
+}
+
+}  // extern "C"

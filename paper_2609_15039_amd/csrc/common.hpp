@@ -1,0 +1,69 @@
+// Shared device/host helpers of the HIP library (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/splitee.h"
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+namespace splitee {
+
+// binary32 -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t bf16_bits_rne(float x)
+{
+    uint32_t b = __float_as_uint(x);
+    if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu)) return (b >> 16) | 0x40u;
+    return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Split binary32 x into hi + mid + lo bfloat16 terms that sum to x exactly.
+__device__ __forceinline__ void split3_bf16(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo)
+{
+    hi = bf16_bits_rne(x);
+    float r1 = x - bf16_bits_to_f32(hi);   // exact in binary32
+    mid = bf16_bits_rne(r1);
+    float r2 = r1 - bf16_bits_to_f32(mid); // exact in binary32
+    lo = bf16_bits_rne(r2);                // exact: r2 has at most 8 significant bits
+}
+
+// Workgroup-id remap so that consecutive logical tiles land on the same XCD.
+// The dispatcher places workgroup b on XCD (b mod 8); tiles that share operands
+// are given consecutive logical ids and thus share that XCD's L2.
+__device__ __forceinline__ uint32_t xcd_logical_block(uint32_t b, uint32_t nblocks)
+{
+    const uint32_t nx = 8;
+    uint32_t per = nblocks / nx;
+    uint32_t full = per * nx;
+    if (b >= full) return b;
+    return (b % nx) * per + b / nx;
+}
+
+}  // namespace splitee
+
+// host-side launch helpers implemented in the kernel translation units
+namespace splitee_host {
+int launch_noise(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech, double scale,
+                 uint64_t seed, uint64_t sid, uint64_t row0, hipStream_t s);
+int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int gen_mech,
+                double scale, uint64_t seed, uint64_t sid, uint64_t row0, void* Xt, int prec,
+                int64_t ldxt, int64_t plane_stride, int64_t M, int64_t K,
+                unsigned* zero_ptr, int64_t zero_count, hipStream_t s);
+int launch_unmask(const float* R, int64_t ldr, const float* C, int64_t ldc, float* Y, int64_t ldy,
+                  int64_t M, int64_t N, hipStream_t s);
+int launch_transform_probe(const uint32_t* w, int64_t n, int fn, int force_slow, float* out,
+                           hipStream_t s);
+// Tiled MFMA GEMM: Out = A . W^T (- C if C != nullptr), A given as prec planes.
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);
+int launch_gemm(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
+                int w_type, int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo,
+                int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
+int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
+                  int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,
+                  int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+}  // namespace splitee_host

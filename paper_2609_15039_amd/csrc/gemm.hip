@@ -1,0 +1,665 @@
+// MFMA GEMM kernels of the masked linear layer (gfx950).
+//
+//   Out = A . W^T            (R, the GPU's part: r = W (x + eta))
+//   Out = fl32(A . W^T - C)  (fused unmask epilogue, Eq. add-and-then-subtract)
+//
+// A is the masked input in one of three forms: float32 (binary32 MFMA
+// v_mfma_f32_16x16x4_f32), one bfloat16 plane, or three bfloat16 planes
+// hi + mid + lo that sum exactly to the float32 masked input (three bfloat16
+// MFMA passes v_mfma_f32_16x16x32_bf16 into one float32 accumulator).  W is
+// N x K row-major (nn.Linear layout), float32 or bfloat16.
+//
+// Tiling: a workgroup owns a BM x BN output tile and a contiguous range of K
+// tiles; 16-byte global loads are staged through padded LDS rows (16 bytes of
+// padding keeps the 16-byte fragment reads conflict-free), the next K tile is
+// prefetched into registers while the current one is multiplied.  When the
+// K range is split over several workgroups (split-K, to fill 256 CUs at small
+// M), each writes its float32 partial tile to the workspace and the last one to
+// arrive (device-scope counter) sums the partials in split order and applies
+// the epilogue, so results do not depend on arrival order.
+#include "common.hpp"
+
+namespace {
+
+constexpr int WAVE = 64;
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// Epilogue for one accumulator element: the split-K partial or the final value.
+struct TileCtx {
+    int m0, n0, M, N;
+    const float* C; int64_t ldc;
+    float* Out; int64_t ldo;
+};
+
+__device__ __forceinline__ void store_final(const TileCtx& t, int row, int col, float v)
+{
+    if (row < t.M && col < t.N) {
+        if (t.C) v = v - t.C[(int64_t)row * t.ldc + col];
+        t.Out[(int64_t)row * t.ldo + col] = v;
+    }
+}
+
+// Split-K hand-off between the workgroups of one output tile.  Partials are
+// written and read with agent-scope relaxed atomic accesses, which gfx950 performs
+// write-through / coherently (sc1) across the XCDs' L2 caches.  Each wave waits
+// for its partial stores to complete before the workgroup bumps the tile
+// counter, so the workgroup that sees the count reach ksplit-1 reads complete
+// partials.  This is the ordering of an agent-scope release/acquire pair
+// without its whole-L2 write-back and invalidate, which only non-coherent
+// stores need.
+__device__ __forceinline__ void store_partial(float* p, float v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_partial(const float* p)
+{
+    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Returns true in the last-arriving workgroup of the tile (all its threads),
+// which then owns the reduction and resets the counter for the next call.
+// `flag` is one LDS word the workgroup no longer needs for anything else.
+__device__ __forceinline__ bool splitk_arrive(unsigned* counter, int ksplit, unsigned* flag)
+{
+    __builtin_amdgcn_s_waitcnt(0); // this wave's partial stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag = (prev == (unsigned)(ksplit - 1)) ? 1u : 0u;
+    }
+    __syncthreads();
+    return *flag != 0u;
+}
+
+// The last workgroup's reduction of a BM x BN tile: the tile is walked row-major
+// in 16-byte units, CH per thread at a time; for each chunk all loads of one
+// split are issued together (agent-coherent buffer loads, sc1), then added in
+// split order, then C is subtracted and Y stored with 16-byte accesses.
+template <int BM, int BN, int NT, int CH>
+__device__ __forceinline__ void splitk_reduce(const float* tp, int ksplit, int m0, int n0, int M, int N,
+                                              const float* C, int64_t ldc, float* Out, int64_t ldo)
+{
+    constexpr int F4 = BM * BN / 4, ROW4 = BN / 4;
+    static_assert(F4 % (NT * CH) == 0, "reduction chunks");
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(tp), (short)0,
+                                                                       ksplit * BM * BN * 4, 0x00020000);
+    constexpr int SC1 = 16; // cache policy: coherent at agent scope
+    for (int c0 = 0; c0 < F4; c0 += NT * CH) {
+        f32x4_t sum[CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+            sum[c] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                rp, (c0 + c * NT + (int)threadIdx.x) * 16, 0, SC1));
+        for (int q = 1; q < ksplit; ++q) {
+            f32x4_t v[CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c)
+                v[c] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                    rp, (q * F4 + c0 + c * NT + (int)threadIdx.x) * 16, 0, SC1));
+#pragma unroll
+            for (int c = 0; c < CH; ++c) sum[c] += v[c];
+        }
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int f = c0 + c * NT + (int)threadIdx.x;
+            const int row = m0 + f / ROW4, col = n0 + (f % ROW4) * 4;
+            if (row >= M) continue;
+            f32x4_t y = sum[c];
+            if (col + 4 <= N) {
+                if (C) y -= __builtin_bit_cast(f32x4_t, *reinterpret_cast<const float4*>(C + (int64_t)row * ldc + col));
+                *reinterpret_cast<float4*>(Out + (int64_t)row * ldo + col) = __builtin_bit_cast(float4, y);
+            } else {
+                for (int e = 0; e < 4 && col + e < N; ++e) {
+                    float v = y[e];
+                    if (C) v = v - C[(int64_t)row * ldc + col + e];
+                    Out[(int64_t)row * ldo + col + e] = v;
+                }
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void splitk_reset(unsigned* counter)
+{
+    __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// --------------------------------------------------------------- bf16 MFMA
+// A K tile is 64 bf16 = 8 units of 16 bytes per row.  Tiles are fetched with
+// bounds-checked buffer loads (lanes whose row or k lies outside the matrix get
+// an offset beyond the buffer's extent and read zeros, which pads every tail)
+// into two register sets, so two K tiles are in flight while a third is
+// multiplied out of LDS.  LDS holds two stages; unit kc of row r sits at slot
+// kc ^ (r & 7), so the 16-byte fragment reads of 8 consecutive rows and the
+// stores of consecutive lanes are bank-conflict free.  One barrier per K tile.
+
+constexpr int BK = 64;
+constexpr uint32_t OOB = 0x80000000u;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff)
+{
+    u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+template <int NPL, int BM, int BN, int WGM, int WGN>
+__global__ void __launch_bounds__(WGM * WGN * WAVE)
+gemm_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
+                 const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
+                 float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
+                 int ksplit, int kt_per_split, float* __restrict__ part, unsigned* __restrict__ counters)
+{
+    constexpr int NW = WGM * WGN;
+    constexpr int WTM = BM / WGM, WTN = BN / WGN;
+    constexpr int TM = WTM / 16, TN = WTN / 16;
+    constexpr int ROWS = NPL * BM + BN;          // LDS rows of 128 bytes per stage
+    constexpr int STAGE_BYTES = ROWS * 128;
+    constexpr int UNITS = ROWS * 8;
+    static_assert(UNITS % (NW * WAVE) == 0, "stage must split evenly over the threads");
+    constexpr int LPT = UNITS / (NW * WAVE);     // 16-byte loads per thread per stage
+    static_assert(TM * 16 == WTM && TN * 16 == WTN, "wave tile");
+
+    __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE_BYTES];
+
+    const int tid = threadIdx.x, lane = tid % WAVE;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
+    const int wm = wave % WGM, wn = wave / WGM;
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int tiles = mtiles * ntiles;
+    const int split = (int)lb / tiles, tile = (int)lb % tiles;
+    const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
+    const int ktiles = (K + BK - 1) / BK;
+    const int kt0 = split * kt_per_split;
+    const int kt1 = min(kt0 + kt_per_split, ktiles);
+    const int nk = kt1 > kt0 ? kt1 - kt0 : 0;
+
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
+
+    // unit u = tid + t * NT of the stage: row u / 8, slot u % 8, k chunk slot ^ (row & 7)
+    uint32_t goff[LPT];
+    int gkc[LPT];
+#pragma unroll
+    for (int t = 0; t < LPT; ++t) {
+        const int u = tid + t * NW * WAVE;
+        const int row = u >> 3, kc = (u & 7) ^ (row & 7);
+        gkc[t] = kc * 8;
+        if (row < NPL * BM) {
+            const int p = row / BM, r = row - p * BM, gm = m0 + r;
+            goff[t] = gm < M ? (uint32_t)((p * pstride + (int64_t)gm * lda) * 2 + kc * 16) : OOB;
+        } else {
+            const int gn = n0 + row - NPL * BM;
+            goff[t] = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + kc * 16) : OOB;
+        }
+    }
+    // Loads are issued unconditionally (tiles past this split's range read zeros)
+    // so the compiler can count the loads in flight and wait only for the oldest.
+    auto gload = [&](int kt, uint4 (&rg)[LPT]) {
+        const int kb = kt * BK;
+        const bool live = kt < kt1;
+#pragma unroll
+        for (int t = 0; t < LPT; ++t) {
+            const uint32_t off = (live && goff[t] != OOB && kb + gkc[t] < K) ? goff[t] + (uint32_t)kb * 2 : OOB;
+            // a wave's 64 units lie in 8 whole rows, all of A or all of W
+            if ((wave + t * NW) * WAVE < NPL * BM * 8) rg[t] = load16(ra, off);
+            else rg[t] = load16(rw, off);
+        }
+    };
+    auto swrite = [&](int stage, const uint4 (&rg)[LPT]) {
+        unsigned char* sb = smem + stage * STAGE_BYTES;
+#pragma unroll
+        for (int t = 0; t < LPT; ++t)
+            *reinterpret_cast<uint4*>(sb + (tid + t * NW * WAVE) * 16) = rg[t];
+    };
+
+    f32x4_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    uint4 r0[LPT], r1[LPT];
+    gload(kt0, r0);
+    gload(kt0 + 1, r1);
+    swrite(0, r0);
+    __syncthreads();
+
+    const int fr = lane % 16, fq = lane / 16;
+    auto compute = [&](int stage) {
+        const unsigned char* sb = smem + stage * STAGE_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int kc = ks * 4 + fq;
+            bf16x8_t bfr[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = NPL * BM + wn * WTN + j * 16 + fr;
+                bfr[j] = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ (r & 7)) << 4)));
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+#pragma unroll
+                for (int p = 0; p < NPL; ++p) {
+                    const int r = p * BM + wm * WTM + i * 16 + fr;
+                    const bf16x8_t af = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ (r & 7)) << 4)));
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], acc[i][j], 0, 0, 0);
+                }
+            }
+        }
+    };
+
+    // tiles go to stages 0,1,0,1,...; while stage (it % 2) is multiplied, the
+    // next tile waits in registers and the one after is being fetched
+    int it = 0;
+    // (sched_barrier keeps the prefetch ahead of the MFMAs it overlaps)
+    for (; it + 1 < nk; it += 2) {
+        gload(kt0 + it + 2, r0);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(0);
+        swrite(1, r1);
+        __syncthreads();
+        gload(kt0 + it + 3, r1);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(1);
+        swrite(0, r0);
+        __syncthreads();
+    }
+    if (it < nk) compute(0);
+
+    // accumulator element r of fragment (i, j): row 4*(lane/16) + r, column lane%16
+    TileCtx t{m0, n0, M, N, C, ldc, Out, ldo};
+    const int erow = 4 * (lane / 16), ecol = lane % 16;
+    if (ksplit == 1) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    store_final(t, m0 + wm * WTM + i * 16 + erow + r, n0 + wn * WTN + j * 16 + ecol, acc[i][j][r]);
+        return;
+    }
+    float* mypart = part + ((int64_t)tile * ksplit + split) * (BM * BN);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                store_partial(&mypart[(wm * WTM + i * 16 + erow + r) * BN + wn * WTN + j * 16 + ecol], acc[i][j][r]);
+    if (!splitk_arrive(counters + tile, ksplit, reinterpret_cast<unsigned*>(smem))) return;
+    splitk_reduce<BM, BN, NW * WAVE, (BM * BN / 4 / (NW * WAVE) < 8 ? BM * BN / 4 / (NW * WAVE) : 8)>(part + (int64_t)tile * ksplit * (BM * BN), ksplit, m0, n0, M, N, C,
+                                          ldc, Out, ldo);
+    if (tid == 0) splitk_reset(counters + tile);
+}
+
+// --------------------------------------------------------------- f32 MFMA
+// v_mfma_f32_16x16x4_f32 takes one k per lane group; four instructions cover a
+// 16-wide k slice whose elements are assigned so that each lane reads one
+// 16-byte run (k = 4 * (lane/16) + j in instruction j), identically for A and W.
+
+template <int BM, int BN, int BK, int WGM, int WGN, bool WBF16>
+__global__ void __launch_bounds__(WGM * WGN * WAVE)
+gemm_f32_kernel(const float* __restrict__ A, int64_t lda, const void* __restrict__ Wv, int64_t ldw,
+                const float* __restrict__ C, int64_t ldc, float* __restrict__ Out, int64_t ldo, int M,
+                int N, int K, int mtiles, int ntiles, int ksplit, int kt_per_split,
+                float* __restrict__ part, unsigned* __restrict__ counters)
+{
+    constexpr int NT = WGM * WGN * WAVE;
+    constexpr int LDK = BK + 4;
+    constexpr int WTM = BM / WGM, WTN = BN / WGN;
+    constexpr int TM = WTM / 16, TN = WTN / 16;
+    constexpr int CPR = BK / 4;                  // 16-byte float chunks per row
+    constexpr int WCPR = WBF16 ? BK / 8 : BK / 4; // 16-byte W chunks per row
+    constexpr int ACH = BM * CPR / NT, BCH = BN * WCPR / NT;
+    static_assert(ACH * NT == BM * CPR && BCH * NT == BN * WCPR, "tile/thread mismatch");
+    static_assert(BK % 16 == 0, "k tile");
+
+    __shared__ __attribute__((aligned(16))) float sA[BM * LDK];
+    __shared__ __attribute__((aligned(16))) float sB[BN * LDK];
+
+    const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+    const int wm = wave % WGM, wn = wave / WGM;
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int tiles = mtiles * ntiles;
+    const int split = (int)lb / tiles, tile = (int)lb % tiles;
+    const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
+    const int ktiles = (K + BK - 1) / BK;
+    const int kt0 = split * kt_per_split;
+    const int kt1 = min(kt0 + kt_per_split, ktiles);
+
+    uint4 ra[ACH], rb[BCH];
+    auto gload = [&](int kt) {
+        const int kb = kt * BK;
+#pragma unroll
+        for (int c = 0; c < ACH; ++c) {
+            const int idx = tid + c * NT, row = idx / CPR, col = (idx % CPR) * 4;
+            const int gm = m0 + row, gk = kb + col;
+            ra[c] = (gm < M && gk < K) ? *reinterpret_cast<const uint4*>(A + (int64_t)gm * lda + gk)
+                                       : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int c = 0; c < BCH; ++c) {
+            const int idx = tid + c * NT, row = idx / WCPR, col = (idx % WCPR) * (WBF16 ? 8 : 4);
+            const int gn = n0 + row, gk = kb + col;
+            const bool ok = gn < N && gk < K;
+            if (WBF16)
+                rb[c] = ok ? *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(Wv) + (int64_t)gn * ldw + gk)
+                           : make_uint4(0, 0, 0, 0);
+            else
+                rb[c] = ok ? *reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(Wv) + (int64_t)gn * ldw + gk)
+                           : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto swrite = [&]() {
+#pragma unroll
+        for (int c = 0; c < ACH; ++c) {
+            const int idx = tid + c * NT, row = idx / CPR, col = (idx % CPR) * 4;
+            *reinterpret_cast<uint4*>(&sA[row * LDK + col]) = ra[c];
+        }
+#pragma unroll
+        for (int c = 0; c < BCH; ++c) {
+            const int idx = tid + c * NT, row = idx / WCPR, col = (idx % WCPR) * (WBF16 ? 8 : 4);
+            if (WBF16) {
+                // bfloat16 -> float32 is exact: the 16 bits become the upper half
+                const uint4 v = rb[c];
+                uint4 lo = make_uint4(v.x << 16, v.x & 0xFFFF0000u, v.y << 16, v.y & 0xFFFF0000u);
+                uint4 hi = make_uint4(v.z << 16, v.z & 0xFFFF0000u, v.w << 16, v.w & 0xFFFF0000u);
+                *reinterpret_cast<uint4*>(&sB[row * LDK + col]) = lo;
+                *reinterpret_cast<uint4*>(&sB[row * LDK + col + 4]) = hi;
+            } else {
+                *reinterpret_cast<uint4*>(&sB[row * LDK + col]) = rb[c];
+            }
+        }
+    };
+
+    f32x4_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const int frow = lane % 16, fk = (lane / 16) * 4;
+    if (kt0 < kt1) gload(kt0);
+    for (int kt = kt0; kt < kt1; ++kt) {
+        __syncthreads();
+        swrite();
+        __syncthreads();
+        if (kt + 1 < kt1) gload(kt + 1);
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            float4 af[TM], bfr[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                af[i] = *reinterpret_cast<const float4*>(&sA[(wm * WTM + i * 16 + frow) * LDK + ks * 16 + fk]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                bfr[j] = *reinterpret_cast<const float4*>(&sB[(wn * WTN + j * 16 + frow) * LDK + ks * 16 + fk]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].x, bfr[j].x, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].y, bfr[j].y, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].z, bfr[j].z, acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bfr[j].w, acc[i][j], 0, 0, 0);
+                }
+        }
+    }
+
+    TileCtx t{m0, n0, M, N, C, ldc, Out, ldo};
+    const int erow = 4 * (lane / 16), ecol = lane % 16;
+    if (ksplit == 1) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    store_final(t, m0 + wm * WTM + i * 16 + erow + r, n0 + wn * WTN + j * 16 + ecol, acc[i][j][r]);
+        return;
+    }
+    float* mypart = part + ((int64_t)tile * ksplit + split) * (BM * BN);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                store_partial(&mypart[(wm * WTM + i * 16 + erow + r) * BN + wn * WTN + j * 16 + ecol], acc[i][j][r]);
+    if (!splitk_arrive(counters + tile, ksplit, reinterpret_cast<unsigned*>(sA))) return;
+    splitk_reduce<BM, BN, WGM * WGN * WAVE, (BM * BN / 4 / (WGM * WGN * WAVE) < 8 ? BM * BN / 4 / (WGM * WGN * WAVE) : 8)>(part + (int64_t)tile * ksplit * (BM * BN), ksplit, m0, n0, M, N, C,
+                                          ldc, Out, ldo);
+    if (tid == 0) splitk_reset(counters + tile);
+}
+
+// --------------------------------------------------------- skinny (M <= 16)
+// Decode-shaped GEMM: W is streamed once straight into MFMA registers (no LDS);
+// the masked-input fragments (at most 16 rows) are read through the cache.  A
+// workgroup is 4 waves x 16 output columns; each wave walks its K range in
+// 32-wide steps, KU steps per batch of loads.
+
+template <int NPL, int KU>
+__global__ void __launch_bounds__(256)
+skinny_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
+              const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
+              float* __restrict__ Out, int64_t ldo, int M, int N, int K, int ntiles, int ksplit,
+              int ks_per_split, float* __restrict__ part, unsigned* __restrict__ counters)
+{
+    constexpr int BN = 64;
+    const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int split = (int)lb / ntiles, tile = (int)lb % ntiles;
+    const int n0 = tile * BN;
+    const int ksteps = (K + 31) / 32;
+    const int s0 = split * ks_per_split, s1 = min(s0 + ks_per_split, ksteps);
+
+    const int frow = lane % 16, fk = (lane / 16) * 8;
+    const int wn_row = n0 + wave * 16 + frow; // W row this lane loads
+    const bool wrow_ok = wn_row < N;
+    const bool arow_ok = frow < M;
+    const uint16_t* wp = W + (int64_t)(wrow_ok ? wn_row : 0) * ldw + fk;
+    const uint16_t* ap = A + (int64_t)(arow_ok ? frow : 0) * lda + fk;
+
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int sb = s0; sb < s1; sb += KU) {
+        uint4 wv[KU];
+        uint4 av[KU][NPL];
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int k = (sb + u) * 32;
+            const bool ok = (sb + u) < s1 && (k + fk) < K;
+            wv[u] = (ok && wrow_ok) ? *reinterpret_cast<const uint4*>(wp + k) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int p = 0; p < NPL; ++p)
+                av[u][p] = (ok && arow_ok) ? *reinterpret_cast<const uint4*>(ap + p * pstride + k)
+                                           : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < KU; ++u)
+#pragma unroll
+            for (int p = 0; p < NPL; ++p)
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[u][p]), as_bf16x8(wv[u]), acc, 0, 0, 0);
+    }
+
+    // accumulator element r: row (token) 4*(lane/16) + r, column n0 + 16*wave + lane%16
+    TileCtx t{0, n0, M, N, C, ldc, Out, ldo};
+    const int erow = 4 * (lane / 16), col = n0 + wave * 16 + lane % 16;
+    if (ksplit == 1) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) store_final(t, erow + r, col, acc[r]);
+        return;
+    }
+    float* mypart = part + ((int64_t)tile * ksplit + split) * (16 * BN);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) store_partial(&mypart[(erow + r) * BN + wave * 16 + lane % 16], acc[r]);
+    __shared__ unsigned flag;
+    if (!splitk_arrive(counters + tile, ksplit, &flag)) return;
+    splitk_reduce<16, BN, 256, 1>(part + (int64_t)tile * ksplit * (16 * BN), ksplit, 0, n0, M, N, C, ldc,
+                                  Out, ldo);
+    if (tid == 0) splitk_reset(counters + tile);
+}
+
+// ------------------------------------------------------------ host planning
+
+struct Plan {
+    int bm, bn, bk;
+    int mtiles, ntiles, ktiles;
+    int ksplit, kt_per_split;
+    size_t part_bytes, counter_bytes;
+    int variant; // which instantiation
+};
+
+constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
+
+Plan plan_tiled(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allow_split)
+{
+    Plan p{};
+    if (prec == SPLITEE_PREC_F32) {
+        p.bm = 128; p.bn = 128; p.bk = 32; p.variant = 0;
+        if (M <= 64) { p.bm = 64; p.bn = 64; p.variant = 1; }
+    } else if (prec == SPLITEE_PREC_BF16X3) {
+        p.bm = 64; p.bn = 128; p.bk = 64; p.variant = 0;
+    } else {
+        p.bm = 128; p.bn = 128; p.bk = 64; p.variant = 0;
+        if (M <= 64) { p.bm = 64; p.bn = 128; p.variant = 1; }
+    }
+    (void)w_type;
+    p.mtiles = (int)((M + p.bm - 1) / p.bm);
+    p.ntiles = (int)((N + p.bn - 1) / p.bn);
+    p.ktiles = (int)((K + p.bk - 1) / p.bk);
+    int tiles = p.mtiles * p.ntiles;
+    int ks = 1;
+    if (allow_split && tiles < TARGET_WGS / 2) {
+        ks = (TARGET_WGS / 2 + tiles - 1) / tiles;
+        int max_ks = p.ktiles / 4; // keep at least 4 K tiles per split
+        if (ks > max_ks) ks = max_ks;
+        if (ks < 1) ks = 1;
+    }
+    p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
+    p.ksplit = p.ktiles > 0 ? (p.ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
+    p.counter_bytes = p.ksplit > 1 ? (((size_t)tiles * 4 + 255) / 256) * 256 : 0;
+    p.part_bytes = p.ksplit > 1 ? (size_t)tiles * p.ksplit * p.bm * p.bn * 4 : 0;
+    return p;
+}
+
+Plan plan_skinny(int64_t M, int64_t N, int64_t K)
+{
+    (void)M;
+    Plan p{};
+    p.bm = 16; p.bn = 64; p.bk = 32;
+    p.mtiles = 1;
+    p.ntiles = (int)((N + 63) / 64);
+    p.ktiles = (int)((K + 31) / 32);
+    int ks = (TARGET_WGS + p.ntiles - 1) / p.ntiles;
+    int max_ks = p.ktiles / 8; // at least 8 k-steps per split
+    if (ks > max_ks) ks = max_ks;
+    if (ks < 1) ks = 1;
+    p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
+    p.ksplit = p.ktiles > 0 ? (p.ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
+    p.counter_bytes = p.ksplit > 1 ? (((size_t)p.ntiles * 4 + 255) / 256) * 256 : 0;
+    p.part_bytes = p.ksplit > 1 ? (size_t)p.ntiles * p.ksplit * 16 * 64 * 4 : 0;
+    return p;
+}
+
+}  // namespace
+
+namespace splitee_host {
+
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type)
+{
+    Plan p = plan_tiled(M, N, K, prec, w_type, true);
+    return p.counter_bytes + p.part_bytes;
+}
+
+size_t gemm_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type)
+{
+    return plan_tiled(M, N, K, prec, w_type, true).counter_bytes;
+}
+
+int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const void* W, int w_type,
+                int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,
+                int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    const bool allow_split = ws != nullptr;
+    Plan p = plan_tiled(M, N, K, prec, w_type, allow_split);
+    if (p.ksplit > 1 && ws_bytes < p.counter_bytes + p.part_bytes) return SPLITEE_ERR_WORKSPACE;
+    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
+    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
+    dim3 grid((unsigned)(p.mtiles * p.ntiles * p.ksplit));
+    const int m = (int)M, n = (int)N, k = (int)K;
+    if (prec == SPLITEE_PREC_F32) {
+        const float* a = reinterpret_cast<const float*>(A);
+        if (w_type == SPLITEE_BF16) {
+            if (p.variant == 0)
+                hipLaunchKernelGGL((gemm_f32_kernel<128, 128, 32, 2, 2, true>), grid, dim3(256), 0, s, a, lda, W, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+            else
+                hipLaunchKernelGGL((gemm_f32_kernel<64, 64, 32, 2, 2, true>), grid, dim3(256), 0, s, a, lda, W, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        } else {
+            if (p.variant == 0)
+                hipLaunchKernelGGL((gemm_f32_kernel<128, 128, 32, 2, 2, false>), grid, dim3(256), 0, s, a, lda, W, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+            else
+                hipLaunchKernelGGL((gemm_f32_kernel<64, 64, 32, 2, 2, false>), grid, dim3(256), 0, s, a, lda, W, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        }
+    } else {
+        const uint16_t* a = reinterpret_cast<const uint16_t*>(A);
+        const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+        // the buffer loads address each operand with 31-bit byte offsets
+        const int64_t planes = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
+        if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
+            return SPLITEE_ERR_UNSUPPORTED;
+        if (prec == SPLITEE_PREC_BF16) {
+            if (p.variant == 0)
+                hipLaunchKernelGGL((gemm_bf16_kernel<1, 128, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+            else
+                hipLaunchKernelGGL((gemm_bf16_kernel<1, 64, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        } else {
+            hipLaunchKernelGGL((gemm_bf16_kernel<3, 64, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        }
+    }
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
+
+size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
+{
+    (void)prec;
+    Plan p = plan_skinny(M, N, K);
+    return p.counter_bytes + p.part_bytes;
+}
+
+size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K)
+{
+    return plan_skinny(M, N, K).counter_bytes;
+}
+
+int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const void* W, int64_t ldw,
+                  const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M, int64_t N,
+                  int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (M > 16 || prec == SPLITEE_PREC_F32) return SPLITEE_ERR_UNSUPPORTED;
+    Plan p = plan_skinny(M, N, K);
+    if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
+    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
+    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
+    dim3 grid((unsigned)(p.ntiles * p.ksplit));
+    const uint16_t* a = reinterpret_cast<const uint16_t*>(A);
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+    if (prec == SPLITEE_PREC_BF16)
+        hipLaunchKernelGGL((skinny_kernel<1, 8>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+    else
+        hipLaunchKernelGGL((skinny_kernel<3, 8>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
+
+}  // namespace splitee_host

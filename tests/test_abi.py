@@ -1,0 +1,130 @@
+"""The C-ABI library on the host: it loads, exports every declared entry point,
+and rejects invalid arguments synchronously without touching a device.
+
+The pointers passed here are never dereferenced: every call fails validation
+before any launch (16 is a non-null, 16-byte aligned stand-in address).
+"""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2609_15039_amd as sp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HDR = os.path.join(ROOT, "include", "splitee.h")
+OK, ARG, SHAPE, DTYPE, ALIGN, UNSUP, HIP, WS = 0, -1, -2, -3, -4, -5, -6, -7
+P = 16  # aligned stand-in pointer
+L, G, NONE = 0, 1, 2
+F32, BF16 = 0, 1
+PF, PB, PX = 0, 1, 2
+
+
+def declared_functions():
+    text = open(HDR).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(splitee_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return sp.load()
+
+
+def test_library_exports_every_declared_function(lib):
+    decl = declared_functions()
+    assert set(decl) == set(sp.EXPORTED)
+    for name in decl:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert lib.splitee_abi_version() == 1
+    for code in (OK, ARG, SHAPE, DTYPE, ALIGN, UNSUP, HIP, WS):
+        assert lib.splitee_status_string(code)
+    assert lib.splitee_status_string(12345) == b"unknown status"
+
+
+def noise(lib, eta=P, ld=8, M=2, K=8, mech=L, d=1.0, e=1.0):
+    return lib.splitee_noise_gen(eta, ld, M, K, mech, d, e, 0, 0, 0, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(e=0.0), ARG), (dict(e=-1.0), ARG), (dict(e=math.nan), ARG), (dict(e=math.inf), ARG),
+    (dict(d=-1.0), ARG), (dict(d=math.nan), ARG), (dict(d=math.inf), ARG), (dict(mech=3), ARG),
+    (dict(K=6, ld=8), SHAPE), (dict(ld=4), SHAPE), (dict(M=-1), SHAPE),
+    (dict(eta=8), ALIGN), (dict(ld=10, K=8), ALIGN), (dict(eta=None), ARG),
+    (dict(M=0), OK), (dict(K=0, ld=0), OK)])
+def test_noise_gen_validation(lib, kw, code):
+    assert noise(lib, **kw) == code
+
+
+def test_mask_validation(lib):
+    f = lib.splitee_mask
+    assert f(P, 8, P, 8, P, 7, 8, 2, 8, None) == UNSUP
+    assert f(P, 8, P, 8, P, PF, 8, 2, 6, None) == SHAPE
+    assert f(P, 4, P, 8, P, PF, 8, 2, 8, None) == SHAPE
+    assert f(P, 8, None, 8, P, PF, 8, 2, 8, None) == ARG
+    assert f(P, 8, P, 8, 8, PF, 8, 2, 8, None) == ALIGN
+    assert f(P, 8, P, 8, P, PB, 12, 2, 8, None) == ALIGN  # 24-byte bf16 row pitch
+    assert f(P, 8, P, 8, P, PB, 8, 0, 8, None) == OK
+
+
+def test_masked_linear_validation(lib):
+    f = lib.splitee_masked_linear
+    assert f(P, PX, 8, P, F32, 8, P, 8, 2, 8, 8, None) == UNSUP  # BF16X3 needs bf16 W
+    assert f(P, PB, 8, P, F32, 8, P, 8, 2, 8, 8, None) == UNSUP
+    assert f(P, PF, 8, P, 5, 8, P, 8, 2, 8, 8, None) == DTYPE
+    assert f(P, PF, 4, P, F32, 4, P, 4, 2, 4, 4, None) == SHAPE  # K % 8
+    assert f(P, PF, 8, P, F32, 8, P, 4, 2, 8, 8, None) == SHAPE  # ldr < N
+    assert f(P, PF, 8, 4, F32, 8, P, 8, 2, 8, 8, None) == ALIGN
+    assert f(P, PF, 8, P, F32, 8, P, 8, 0, 8, 8, None) == OK
+
+
+def test_unmask_validation(lib):
+    f = lib.splitee_unmask
+    assert f(P, 4, P, 8, P, 8, 2, 8, None) == SHAPE
+    assert f(P, 8, P, 8, 4, 8, 2, 8, None) == ALIGN
+    assert f(P, 8, None, 8, P, 8, 2, 8, None) == ARG
+    assert f(P, 8, P, 8, P, 8, 2, 0, None) == OK
+
+
+def fused(lib, X=P, W=P, wt=BF16, C=P, Y=P, M=2, N=8, K=8, mech=G, d=1.0, e=1.0, prec=PX,
+          ws=256, wsb=1 << 20, eta=None):
+    return lib.splitee_masked_linear_fused(X, K, W, wt, K, C, N, Y, N, M, N, K, mech, d, e, 0, 0, 0,
+                                           eta, prec, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(e=0.0), ARG), (dict(d=-2.0), ARG), (dict(mech=9), ARG), (dict(prec=3), UNSUP),
+    (dict(wt=F32), UNSUP), (dict(wt=F32, prec=PB), UNSUP), (dict(wt=4, prec=PF), DTYPE),
+    (dict(K=4), SHAPE), (dict(C=None), ARG), (dict(X=None), ARG), (dict(Y=8), ALIGN),
+    (dict(eta=8), ALIGN), (dict(wsb=0), WS), (dict(ws=None), WS), (dict(ws=16), ALIGN),
+    (dict(M=0), OK), (dict(N=0), OK)])
+def test_fused_validation(lib, kw, code):
+    assert fused(lib, **kw) == code
+
+
+def test_correction_validation(lib):
+    f = lib.splitee_correction
+    assert f(P, 8, P, BF16, 8, 2, 8, 8, G, 1.0, 1.0, 0, 0, 0, PB, 256, 1 << 20, None) == UNSUP
+    assert f(P, 8, P, BF16, 8, 2, 8, 8, G, 1.0, 0.0, 0, 0, 0, PX, 256, 1 << 20, None) == ARG
+    assert f(P, 8, P, BF16, 8, 2, 8, 8, G, 1.0, 1.0, 0, 0, 0, PX, 256, 0, None) == WS
+    assert f(P, 8, P, BF16, 8, 0, 8, 8, G, 1.0, 1.0, 0, 0, 0, PX, 256, 0, None) == OK
+
+
+def test_workspace_sizes(lib):
+    q = lib.splitee_fused_workspace_bytes
+    assert q(2, 8, 6, PX) == 0  # K % 8
+    assert q(2, 8, 8, 7) == 0
+    # the masked-input planes alone: 3 x M x K bfloat16, 256-byte rounded
+    assert q(128, 5120, 3072, PX) >= 3 * 128 * 3072 * 2
+    assert q(128, 5120, 3072, PF) >= 128 * 3072 * 4
+    assert q(1, 6144, 2560, PX) % 256 == 0
+
+
+def test_transform_probe_validation(lib):
+    assert lib.splitee_transform_probe(P, 4, 4, 0, P, None) == ARG
+    assert lib.splitee_transform_probe(P, 0, 0, 0, P, None) == OK
