@@ -22,6 +22,7 @@
 namespace {
 
 constexpr int WAVE = 64;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
@@ -125,6 +126,95 @@ __device__ __forceinline__ void splitk_reset(unsigned* counter)
     __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+constexpr int SC1 = 16;  // buffer cache policy: coherent at agent scope (write-through / bypass)
+constexpr int KSMAX = 8; // largest split-K factor of the tiled kernels
+constexpr uint32_t OOB_OFF = 0x80000000u;
+
+// Finishes the workgroup's BM x BN accumulator tile.  The tile goes through LDS
+// (row-major, rows padded by 4 floats) so that every global access below is a
+// 16-byte access of consecutive columns:
+//   ksplit == 1: Y = acc - C;
+//   ksplit  > 1: this split's partial is written (agent-coherent), the tile
+//                counter is bumped, and the last workgroup to arrive loads all
+//                partials in one round, sums them in split order, subtracts C and
+//                stores Y.
+// `lds` must hold BM * (BN + 4) + 1 floats and be free (callers sync first).
+template <int BM, int BN, int NT, int TM, int TN, int WTM, int WTN, int WGM>
+__device__ __forceinline__ void finish_tile(const f32x4_t (&acc)[TM][TN], float* lds, int m0, int n0, int M, int N,
+                                            const float* C, int64_t ldc, float* Out, int64_t ldo, int ksplit,
+                                            int split, int tile, float* part, unsigned* counters)
+{
+    constexpr int LDT = BN + 4;
+    constexpr int ROW4 = BN / 4, F4 = BM * BN / 4, PER = F4 / NT;
+    constexpr int CH = PER < 4 ? PER : 4;
+    static_assert(F4 % NT == 0 && PER % CH == 0, "epilogue split");
+    const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+    const int wm = wave % WGM, wn = wave / WGM;
+    const int erow = 4 * (lane / 16), ecol = lane % 16;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                lds[(wm * WTM + i * 16 + erow + r) * LDT + wn * WTN + j * 16 + ecol] = acc[i][j][r];
+    __syncthreads();
+
+    auto finish4 = [&](int f, f32x4_t y) {
+        const int row = m0 + f / ROW4, col = n0 + (f % ROW4) * 4;
+        if (row >= M) return;
+        if (col + 4 <= N) {
+            if (C) y -= __builtin_bit_cast(f32x4_t, *reinterpret_cast<const float4*>(C + (int64_t)row * ldc + col));
+            *reinterpret_cast<float4*>(Out + (int64_t)row * ldo + col) = __builtin_bit_cast(float4, y);
+        } else {
+            for (int e = 0; e < 4 && col + e < N; ++e) {
+                float v = y[e];
+                if (C) v = v - C[(int64_t)row * ldc + col + e];
+                Out[(int64_t)row * ldo + col + e] = v;
+            }
+        }
+    };
+    auto lds4 = [&](int f) {
+        return *reinterpret_cast<const f32x4_t*>(&lds[(f / ROW4) * LDT + (f % ROW4) * 4]);
+    };
+
+    if (ksplit == 1) {
+#pragma unroll
+        for (int c = 0; c < PER; ++c) finish4(tid + c * NT, lds4(tid + c * NT));
+        return;
+    }
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+        part + (int64_t)tile * ksplit * (BM * BN), (short)0, ksplit * BM * BN * 4, 0x00020000);
+#pragma unroll
+    for (int c = 0; c < PER; ++c) {
+        const int f = tid + c * NT;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, lds4(f)), rp, (split * F4 + f) * 16, 0, SC1);
+    }
+    unsigned* flag = reinterpret_cast<unsigned*>(lds + BM * LDT);
+    if (!splitk_arrive(counters + tile, ksplit, flag)) return;
+#pragma unroll
+    for (int c0 = 0; c0 < PER; c0 += CH) {
+        f32x4_t v[KSMAX][CH];
+#pragma unroll
+        for (int q = 0; q < KSMAX; ++q)
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int f = tid + (c0 + c) * NT;
+                const uint32_t off = q < ksplit ? (uint32_t)((q * F4 + f) * 16) : OOB_OFF;
+                v[q][c] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, (int)off, 0, SC1));
+            }
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            f32x4_t sum = v[0][c];
+#pragma unroll
+            for (int q = 1; q < KSMAX; ++q)
+                if (q < ksplit) sum += v[q][c];
+            finish4(tid + (c0 + c) * NT, sum);
+        }
+    }
+    if (tid == 0) splitk_reset(counters + tile);
+}
+
 // --------------------------------------------------------------- bf16 MFMA
 // A K tile is 64 bf16 = 8 units of 16 bytes per row.  Tiles are fetched with
 // bounds-checked buffer loads (lanes whose row or k lies outside the matrix get
@@ -136,7 +226,6 @@ __device__ __forceinline__ void splitk_reset(unsigned* counter)
 
 constexpr int BK = 64;
 constexpr uint32_t OOB = 0x80000000u;
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes)
 {
@@ -166,7 +255,9 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     constexpr int LPT = UNITS / (NW * WAVE);     // 16-byte loads per thread per stage
     static_assert(TM * 16 == WTM && TN * 16 == WTN, "wave tile");
 
-    __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE_BYTES];
+    // two stages; the epilogue reuses the same memory for the output tile
+    constexpr int SMEM = 2 * STAGE_BYTES > (BM * (BN + 4) + 4) * 4 ? 2 * STAGE_BYTES : (BM * (BN + 4) + 4) * 4;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
 
     const int tid = threadIdx.x, lane = tid % WAVE;
     const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
@@ -275,31 +366,9 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     }
     if (it < nk) compute(0);
 
-    // accumulator element r of fragment (i, j): row 4*(lane/16) + r, column lane%16
-    TileCtx t{m0, n0, M, N, C, ldc, Out, ldo};
-    const int erow = 4 * (lane / 16), ecol = lane % 16;
-    if (ksplit == 1) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    store_final(t, m0 + wm * WTM + i * 16 + erow + r, n0 + wn * WTN + j * 16 + ecol, acc[i][j][r]);
-        return;
-    }
-    float* mypart = part + ((int64_t)tile * ksplit + split) * (BM * BN);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                store_partial(&mypart[(wm * WTM + i * 16 + erow + r) * BN + wn * WTN + j * 16 + ecol], acc[i][j][r]);
-    if (!splitk_arrive(counters + tile, ksplit, reinterpret_cast<unsigned*>(smem))) return;
-    splitk_reduce<BM, BN, NW * WAVE, (BM * BN / 4 / (NW * WAVE) < 8 ? BM * BN / 4 / (NW * WAVE) : 8)>(part + (int64_t)tile * ksplit * (BM * BN), ksplit, m0, n0, M, N, C,
-                                          ldc, Out, ldo);
-    if (tid == 0) splitk_reset(counters + tile);
+    __syncthreads(); // every wave is done with the stage buffers
+    finish_tile<BM, BN, NW * WAVE, TM, TN, WTM, WTN, WGM>(acc, reinterpret_cast<float*>(smem), m0, n0, M, N, C, ldc,
+                                                        Out, ldo, ksplit, split, tile, part, counters);
 }
 
 // --------------------------------------------------------------- f32 MFMA
@@ -543,6 +612,7 @@ Plan plan_tiled(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allo
         ks = (TARGET_WGS / 2 + tiles - 1) / tiles;
         int max_ks = p.ktiles / 4; // keep at least 4 K tiles per split
         if (ks > max_ks) ks = max_ks;
+        if (ks > KSMAX) ks = KSMAX;
         if (ks < 1) ks = 1;
     }
     p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
