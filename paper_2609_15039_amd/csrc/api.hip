@@ -6,7 +6,7 @@
 
 namespace splitee_host {
 size_t gemm_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);
-size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K);
+size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec);
 }
 
 namespace {
@@ -54,7 +54,7 @@ size_t gemm_ws(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 }
 size_t gemm_counters(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
-    return use_skinny(M, prec) ? splitee_host::skinny_counter_bytes(M, N, K)
+    return use_skinny(M, prec) ? splitee_host::skinny_counter_bytes(M, N, K, prec)
                                : splitee_host::gemm_counter_bytes(M, N, K, prec, w_type);
 }
 

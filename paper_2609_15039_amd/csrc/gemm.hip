@@ -512,69 +512,152 @@ gemm_f32_kernel(const float* __restrict__ A, int64_t lda, const void* __restrict
 }
 
 // --------------------------------------------------------- skinny (M <= 16)
-// Decode-shaped GEMM: W is streamed once straight into MFMA registers (no LDS);
-// the masked-input fragments (at most 16 rows) are read through the cache.  A
-// workgroup is 4 waves x 16 output columns; each wave walks its K range in
-// 32-wide steps, KU steps per batch of loads.
+// Decode-shaped GEMM, bound by the single pass over W.  A workgroup owns 64
+// output columns (4 waves x 16) and a range of 32-wide k steps; the number of
+// k splits is the largest that keeps the grid within one round of two
+// workgroups per CU.  The workgroup's slice of the masked input (the M <= 16
+// rows, every plane, this k range) is copied to LDS once; its loads are issued
+// before W's so that they do not queue behind them.  W is streamed from HBM
+// straight into MFMA operand registers through a ring of R k steps per lane.
+// Split-K partials cover rows < M only and are summed in split order by the last
+// workgroup of the tile to arrive.
 
-template <int NPL, int KU>
+constexpr int SK_BN = 64;
+constexpr int SK_RING = 16;
+constexpr int SK_LDS_MAX = 64 * 1024; // masked-input slice per workgroup (two workgroups per CU)
+constexpr int SK_TARGET_WGS = 512;
+constexpr int SK_CP = SK_LDS_MAX / 16 / 256; // slice units per thread (16 at 64 KB)
+
+template <int NPL, int R>
 __global__ void __launch_bounds__(256)
 skinny_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
               const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
               float* __restrict__ Out, int64_t ldo, int M, int N, int K, int ntiles, int ksplit,
-              int ks_per_split, float* __restrict__ part, unsigned* __restrict__ counters)
+              int steps_per_split, float* __restrict__ part, unsigned* __restrict__ counters)
 {
-    constexpr int BN = 64;
-    const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+    extern __shared__ __attribute__((aligned(16))) unsigned char sa[];
+    const int tid = threadIdx.x, lane = tid % WAVE;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
     const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
     const int split = (int)lb / ntiles, tile = (int)lb % ntiles;
-    const int n0 = tile * BN;
+    const int n0 = tile * SK_BN;
     const int ksteps = (K + 31) / 32;
-    const int s0 = split * ks_per_split, s1 = min(s0 + ks_per_split, ksteps);
+    const int s0 = split * steps_per_split;
+    const int ns = max(min(s0 + steps_per_split, ksteps) - s0, 0);
+    const int SA = (steps_per_split + R - 1) / R * R; // steps held in LDS (zero past ns)
+    const int RS = SA * 64 + 16;                      // LDS row pitch; 16 bytes of padding
+    const int fr = lane % 16, fq = lane / 16;
 
-    const int frow = lane % 16, fk = (lane / 16) * 8;
-    const int wn_row = n0 + wave * 16 + frow; // W row this lane loads
-    const bool wrow_ok = wn_row < N;
-    const bool arow_ok = frow < M;
-    const uint16_t* wp = W + (int64_t)(wrow_ok ? wn_row : 0) * ldw + fk;
-    const uint16_t* ap = A + (int64_t)(arow_ok ? frow : 0) * lda + fk;
-
-    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int sb = s0; sb < s1; sb += KU) {
-        uint4 wv[KU];
-        uint4 av[KU][NPL];
+    // 1. slice loads: plane p, row r < M, 16-byte unit c of the row's SA * 64 bytes
+    const int upr = SA * 4, units = NPL * M * upr;
+    uint4 av[SK_CP];
+    {
+        const __amdgpu_buffer_rsrc_t ra =
+            make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
 #pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int k = (sb + u) * 32;
-            const bool ok = (sb + u) < s1 && (k + fk) < K;
-            wv[u] = (ok && wrow_ok) ? *reinterpret_cast<const uint4*>(wp + k) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-            for (int p = 0; p < NPL; ++p)
-                av[u][p] = (ok && arow_ok) ? *reinterpret_cast<const uint4*>(ap + p * pstride + k)
-                                           : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < SK_CP; ++i) {
+            const int u = i * 256 + tid;
+            const int pr = u / upr, c = u - pr * upr;
+            const int p = pr / M, r = pr - p * M;
+            const int k = s0 * 32 + c * 8;
+            const bool ok = u < units && c < ns * 4 && k < K;
+            av[i] = load16(ra, ok ? (uint32_t)((p * pstride + (int64_t)r * lda + k) * 2) : OOB);
         }
-#pragma unroll
-        for (int u = 0; u < KU; ++u)
-#pragma unroll
-            for (int p = 0; p < NPL; ++p)
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[u][p]), as_bf16x8(wv[u]), acc, 0, 0, 0);
     }
 
-    // accumulator element r: row (token) 4*(lane/16) + r, column n0 + 16*wave + lane%16
-    TileCtx t{0, n0, M, N, C, ldc, Out, ldo};
-    const int erow = 4 * (lane / 16), col = n0 + wave * 16 + lane % 16;
-    if (ksplit == 1) {
+    // 2. the W ring
+    const int gn = n0 + wave * 16 + fr;
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
+    const uint32_t wbase = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fq * 16) : OOB;
+    auto wload = [&](int j) {
+        const bool ok = wbase != OOB && j < ns && (s0 + j) * 32 + fq * 8 < K;
+        return load16(rw, ok ? wbase + (uint32_t)(s0 + j) * 64 : OOB);
+    };
+    uint4 ring[R];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) store_final(t, erow + r, col, acc[r]);
+    for (int u = 0; u < R; ++u) ring[u] = wload(u);
+
+    // 3. slice to LDS (waits for the slice loads only: loads complete in order)
+#pragma unroll
+    for (int i = 0; i < SK_CP; ++i) {
+        const int u = i * 256 + tid;
+        if (u < units) {
+            const int pr = u / upr, c = u - pr * upr;
+            *reinterpret_cast<uint4*>(sa + pr * RS + c * 16) = av[i];
+        }
+    }
+    __syncthreads();
+
+    // 4. stream: fragments of step j + 1 are read while step j is multiplied; two
+    // accumulator chains (even / odd steps) so consecutive MFMAs are independent
+    const bool arow = fr < M;
+    auto read_a = [&](int j, bf16x8_t (&a)[NPL]) {
+        const int jj = min(j, SA - 1);
+#pragma unroll
+        for (int p = 0; p < NPL; ++p)
+            a[p] = arow ? as_bf16x8(*reinterpret_cast<const uint4*>(sa + (p * M + fr) * RS + jj * 64 + fq * 16))
+                        : as_bf16x8(make_uint4(0, 0, 0, 0));
+    };
+    f32x4_t acc2[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+    bf16x8_t a[2][NPL];
+    read_a(0, a[0]);
+    const int nloop = (ns + R - 1) / R * R;
+    for (int j = 0; j < nloop; j += R) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            read_a(j + u + 1, a[(u + 1) & 1]);
+#pragma unroll
+            for (int p = 0; p < NPL; ++p)
+                acc2[u & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u & 1][p], as_bf16x8(ring[u]), acc2[u & 1], 0, 0, 0);
+            ring[u] = wload(j + u + R);
+        }
+    }
+    const f32x4_t acc = acc2[0] + acc2[1];
+
+    // 5. epilogue.  Accumulator element r: row 4*(lane/16) + r, column gn.
+    const int erow = 4 * (lane / 16);
+    if (ksplit == 1) {
+        TileCtx t{0, n0, M, N, C, ldc, Out, ldo};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) store_final(t, erow + r, gn, acc[r]);
         return;
     }
-    float* mypart = part + ((int64_t)tile * ksplit + split) * (16 * BN);
+    float* mypart = part + ((int64_t)tile * ksplit + split) * (16 * SK_BN);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) store_partial(&mypart[(erow + r) * BN + wave * 16 + lane % 16], acc[r]);
-    __shared__ unsigned flag;
-    if (!splitk_arrive(counters + tile, ksplit, &flag)) return;
-    splitk_reduce<16, BN, 256, 1>(part + (int64_t)tile * ksplit * (16 * BN), ksplit, 0, n0, M, N, C, ldc,
-                                  Out, ldo);
+    for (int r = 0; r < 4; ++r)
+        if (erow + r < M) store_partial(&mypart[(erow + r) * SK_BN + wave * 16 + fr], acc[r]);
+    if (!splitk_arrive(counters + tile, ksplit, reinterpret_cast<unsigned*>(sa))) return;
+
+    // last workgroup: thread t sums the float4 at row t / 16, columns 4 * (t % 16)..+3
+    // over the splits in split order, eight splits' loads in flight at a time
+    const int row = tid / 16, c4 = (tid % 16) * 4;
+    if (row < M) {
+        const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+            part + (int64_t)tile * ksplit * (16 * SK_BN), (short)0, ksplit * 16 * SK_BN * 4, 0x00020000);
+        f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int q0 = 0; q0 < ksplit; q0 += 8) {
+            f32x4_t v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t off = q0 + i < ksplit ? (uint32_t)(((q0 + i) * 16 * SK_BN + row * SK_BN + c4) * 4) : OOB_OFF;
+                v[i] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, (int)off, 0, SC1));
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (q0 + i < ksplit) sum = (q0 + i == 0) ? v[i] : sum + v[i];
+        }
+        const int gc = n0 + c4;
+        if (gc + 4 <= N) {
+            if (C) sum -= __builtin_bit_cast(f32x4_t, *reinterpret_cast<const float4*>(C + (int64_t)row * ldc + gc));
+            *reinterpret_cast<float4*>(Out + (int64_t)row * ldo + gc) = __builtin_bit_cast(float4, sum);
+        } else {
+            for (int e = 0; e < 4 && gc + e < N; ++e) {
+                float y = sum[e];
+                if (C) y = y - C[(int64_t)row * ldc + gc + e];
+                Out[(int64_t)row * ldo + gc + e] = y;
+            }
+        }
+    }
     if (tid == 0) splitk_reset(counters + tile);
 }
 
@@ -622,22 +705,30 @@ Plan plan_tiled(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allo
     return p;
 }
 
-Plan plan_skinny(int64_t M, int64_t N, int64_t K)
+// Masked-input slice bytes of one skinny workgroup holding `steps` k steps.
+size_t skinny_lds_bytes(int64_t M, int npl, int steps)
 {
-    (void)M;
+    const int sa = (steps + SK_RING - 1) / SK_RING * SK_RING;
+    return (size_t)npl * (size_t)M * (size_t)(sa * 64 + 16);
+}
+
+Plan plan_skinny(int64_t M, int64_t N, int64_t K, int prec)
+{
     Plan p{};
-    p.bm = 16; p.bn = 64; p.bk = 32;
+    const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
+    p.bm = 16; p.bn = SK_BN; p.bk = 32;
     p.mtiles = 1;
-    p.ntiles = (int)((N + 63) / 64);
+    p.ntiles = (int)((N + SK_BN - 1) / SK_BN);
     p.ktiles = (int)((K + 31) / 32);
-    int ks = (TARGET_WGS + p.ntiles - 1) / p.ntiles;
-    int max_ks = p.ktiles / 8; // at least 8 k-steps per split
-    if (ks > max_ks) ks = max_ks;
+    int ks = SK_TARGET_WGS / p.ntiles; // whole rounds only: a partial second round costs a full one
+    if (ks > p.ktiles) ks = p.ktiles;
     if (ks < 1) ks = 1;
-    p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
-    p.ksplit = p.ktiles > 0 ? (p.ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
+    int sps = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
+    while (sps > 1 && skinny_lds_bytes(M > 0 ? M : 1, npl, sps) > (size_t)SK_LDS_MAX) --sps;
+    p.kt_per_split = sps;
+    p.ksplit = p.ktiles > 0 ? (p.ktiles + sps - 1) / sps : 1;
     p.counter_bytes = p.ksplit > 1 ? (((size_t)p.ntiles * 4 + 255) / 256) * 256 : 0;
-    p.part_bytes = p.ksplit > 1 ? (size_t)p.ntiles * p.ksplit * 16 * 64 * 4 : 0;
+    p.part_bytes = p.ksplit > 1 ? (size_t)p.ntiles * p.ksplit * 16 * SK_BN * 4 : 0;
     return p;
 }
 
@@ -702,14 +793,13 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
 
 size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
 {
-    (void)prec;
-    Plan p = plan_skinny(M, N, K);
+    Plan p = plan_skinny(M, N, K, prec);
     return p.counter_bytes + p.part_bytes;
 }
 
-size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K)
+size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec)
 {
-    return plan_skinny(M, N, K).counter_bytes;
+    return plan_skinny(M, N, K, prec).counter_bytes;
 }
 
 int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const void* W, int64_t ldw,
@@ -718,7 +808,12 @@ int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const v
 {
     if (M == 0 || N == 0) return SPLITEE_OK;
     if (M > 16 || prec == SPLITEE_PREC_F32) return SPLITEE_ERR_UNSUPPORTED;
-    Plan p = plan_skinny(M, N, K);
+    const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
+    if ((npl - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
+        return SPLITEE_ERR_UNSUPPORTED;
+    Plan p = plan_skinny(M, N, K, prec);
+    const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
+    if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
     if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
     unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
     float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
@@ -726,9 +821,9 @@ int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const v
     const uint16_t* a = reinterpret_cast<const uint16_t*>(A);
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
     if (prec == SPLITEE_PREC_BF16)
-        hipLaunchKernelGGL((skinny_kernel<1, 8>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        hipLaunchKernelGGL((skinny_kernel<1, SK_RING>), grid, dim3(256), lds, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
     else
-        hipLaunchKernelGGL((skinny_kernel<3, 8>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        hipLaunchKernelGGL((skinny_kernel<3, SK_RING>), grid, dim3(256), lds, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
