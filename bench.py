@@ -15,7 +15,10 @@ at 1024 tokens, and Qwen3-4B decode steps (M tokens at position 1024 of a
 2048-position correction bank).
 
 Prints one JSON line.  Fields beyond the common contract: ``roofline`` (the
-GEMM + unmask kernel, timed per launch with HIP events on its stream),
+GEMM + unmask kernel: each projection group's launches for every layer or
+weight set back to back in one HIP graph, bracketed by HIP events on the stream
+they run on; ``traffic`` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+summary of the workload when the kernel sources still match it, else null),
 ``cpu_baseline`` (the CPU oracle on a bounded sample of the same workload),
 ``modes`` (other precision modes), ``correction_ms`` (offline precompute).
 """
@@ -48,6 +51,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (HBM counter calibration) and exit")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample")
     return ap.parse_args()
@@ -129,24 +134,22 @@ class Path:
         torch.cuda.synchronize()
         self.correction_ms = (time.perf_counter() - t0) * 1e3 / nlayers * self.layers_per_step
 
-    def launches(self, s, events=None):
+    def gemm(self, l, i):
+        """The GEMM + unmask launch of projection group i of layer (or weight set) l."""
+        p, M = self.projs[i], self.M
+        W, C = self.W[l][i], self.C[l][i]
+        self.sp.splitee_masked_linear_unmask(self.Xt[i], self.prec, p.K, W, self.wt, p.K, C, C.stride(0),
+                                             self.Y[i], p.N, M, p.N, p.K, self.ws[i][0], self.ws[i][1])
+
+    def launches(self, s):
         """All kernels of step s (noise + mask, then GEMM + unmask, per projection)."""
         sp, M = self.sp, self.M
         base = (s % self.nsets) * self.layers_per_step
-        nproj = len(self.projs)
         for l in range(base, base + self.layers_per_step):
             for i, p in enumerate(self.projs):
-                X, Xt, Y = self.X[i], self.Xt[i], self.Y[i]
-                sp.splitee_noise_mask(X, p.K, Xt, self.prec, p.K, M, p.K, self.mech, self.delta,
-                                      self.eps, 0, self.sid[l][i], self.row0)
-                e = 2 * ((l - base) * nproj + i)
-                if events is not None:
-                    events[e].record()
-                W, C = self.W[l][i], self.C[l][i]
-                sp.splitee_masked_linear_unmask(Xt, self.prec, p.K, W, self.wt, p.K, C, C.stride(0), Y,
-                                                p.N, M, p.N, p.K, self.ws[i][0], self.ws[i][1])
-                if events is not None:
-                    events[e + 1].record()
+                sp.splitee_noise_mask(self.X[i], p.K, self.Xt[i], self.prec, p.K, M, p.K, self.mech,
+                                      self.delta, self.eps, 0, self.sid[l][i], self.row0)
+                self.gemm(l, i)
 
     def flops(self):
         return self.layers_per_step * sum(2.0 * self.M * p.N * p.K for p in self.projs)
@@ -190,23 +193,38 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
 
-    # per-launch durations of the GEMM + unmask kernel: HIP events recorded on the
-    # stream the kernels run on, around every launch of an eager pass of as many
-    # steps; averaged per projection group over steps and layers
-    nproj, L = len(path.projs), path.layers_per_step
+    # per-launch duration of the GEMM + unmask kernel of each projection group: its
+    # launches for every layer / weight set of the run, back to back in one HIP
+    # graph (eager launches when --no-graph), bracketed by HIP events recorded on
+    # the stream the kernels run on; averaged over launches and repeats
+    nproj = len(path.projs)
     per_proj_us = [0.0] * nproj
-    evs = []
-    torch.cuda.synchronize()
-    for s in range(steps):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * nproj * L)]
-        path.launches(s, e)
-        evs.append(e)
-    torch.cuda.synchronize()
-    for e in evs:
-        for l in range(L):
-            for i in range(nproj):
-                k = 2 * (l * nproj + i)
-                per_proj_us[i] += e[k].elapsed_time(e[k + 1]) * 1e3 / (steps * L)
+    reps = max(2, min(steps, 20))
+    for i in range(nproj):
+        def gemms(i=i):
+            for s in range(path.nsets):
+                base = s * path.layers_per_step
+                for l in range(base, base + path.layers_per_step):
+                    path.gemm(l, i)
+        n_launch = path.nsets * path.layers_per_step
+        if graphs is not None:
+            gemms()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                gemms()
+            go = g.replay
+        else:
+            go = gemms
+        go()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            go()
+        e1.record()
+        torch.cuda.synchronize()
+        per_proj_us[i] = e0.elapsed_time(e1) * 1e3 / (reps * n_launch)
     return path, ms, per_proj_us
 
 
@@ -235,15 +253,62 @@ def cpu_baseline(WL, target_s, projs, tokens, w_dtype):
             O.unmask(R, C)
         return time.perf_counter() - t0
 
-    run(1)
-    t1 = run(2)
-    rows = int(max(1, min(tokens, 2 * target_s / max(t1, 1e-3))))
-    t = run(rows)
-    flops = sum(2.0 * rows * p.N * p.K for p in projs)
-    return {"value": flops / t / 1e12, "unit": "TFLOP/s",
+    run(1)  # warm-up (library loads, first-touch)
+    r0 = min(tokens, 8)
+    per_row = run(r0) / r0  # includes the per-call fixed cost, so rows is not overestimated
+    rows = int(max(1, min(tokens, target_s / 2 / per_row)))
+    total, reps = 0.0, 0
+    while reps == 0 or (total < target_s and reps < 100):
+        total += run(rows)
+        reps += 1
+    flops = reps * sum(2.0 * rows * p.N * p.K for p in projs)
+    return {"value": flops / total / 1e12, "unit": "TFLOP/s",
             "cores": int(max(O.num_threads(), blas_threads)), "kind": "oracle",
-            "sample": "%d of %d tokens of one layer's %d projection group(s): noise, mask, GEMM, "
-                      "correction GEMM, unmask; %.1f s" % (rows, tokens, len(projs), t)}
+            "sample": "%d x %d of %d tokens of one layer's %d projection group(s): noise, mask, GEMM, "
+                      "correction GEMM, unmask; %.1f s" % (reps, rows, tokens, len(projs), total)}
+
+
+def gemm_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, prec_name, names):
+    """HBM bytes per GEMM + unmask launch from the committed rocprofv3 counter
+    summary of this workload (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's
+    readings), or None when there is none or the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.md" % (workload, prec_name))
+    if not os.path.exists(path):
+        return None
+    sha, rows = None, {}
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("source-sha256:"):
+                sha = line.split(":", 1)[1].strip()
+            cells = [c.strip() for c in line.strip().strip("|").split("|")]
+            if len(cells) >= 7 and cells[0] in names:
+                try:
+                    rows[cells[0]] = float(cells[6])
+                except ValueError:
+                    pass
+    if sha != gemm_source_sha() or set(rows) != set(names):
+        return None
+    return rows
+
+
+def copy_probe(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(2):
+        torch.mul(x, 1.0, out=y)  # reads mib MiB, writes mib MiB
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_mib": mib, "read_bytes": n * 4, "write_bytes": n * 4}), flush=True)
 
 
 def main():
@@ -254,6 +319,9 @@ def main():
               "(multi-GPU sharding is a design note, not part of this build); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
     import torch
     import paper_2609_15039_amd as sp
     import workloads as WL
@@ -280,7 +348,12 @@ def main():
         achieved = sum(gflops) / (gemm_us * 1e-6) / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                     "frac": round(achieved / peak, 4)}
-    roofline.update({"traffic": None, "kernel": "GEMM + unmask (one launch per projection group)",
+    pname = {v: k for k, v in sp.PRECS.items()}[prec]
+    names = [p.name for p in path.projs]
+    traffic = measured_traffic(args.workload, pname, names)
+    roofline.update({"traffic": None if traffic is None else int(sum(traffic.values())),
+                     "traffic_per_launch": traffic and {k: int(v) for k, v in traffic.items()},
+                     "kernel": "GEMM + unmask (one launch per projection group)",
                      "launch_us": {p.name: round(u, 2) for p, u in zip(path.projs, per_proj_us)},
                      "bytes_per_launch": {p.name: int(b) for p, b in zip(path.projs, gb)},
                      "flops_per_launch": {p.name: int(f) for p, f in zip(path.projs, gflops)},
@@ -295,7 +368,6 @@ def main():
             modes[mname] = {"ms_per_step": round(m_ms, 4),
                             "tflops": round(flops / (m_ms * 1e-3) / 1e12, 2),
                             "gemm_us": {p.name: round(u, 2) for p, u in zip(path.projs, m_pp)}}
-    pname = {v: k for k, v in sp.PRECS.items()}[prec]
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
