@@ -268,6 +268,9 @@ def cpu_baseline(WL, target_s, projs, tokens, w_dtype):
                       "correction GEMM, unmask; %.1f s" % (reps, rows, tokens, len(projs), total)}
 
 
+GEMM_SOURCES = ["paper_2609_15039_amd/csrc/gemm.hip", "paper_2609_15039_amd/csrc/common.hpp"]
+
+
 def gemm_source_sha():
     import hashlib
     h = hashlib.sha256()
