@@ -19,6 +19,8 @@
 // the epilogue, so results do not depend on arrival order.
 #include "common.hpp"
 
+#include <type_traits>
+
 namespace {
 
 constexpr int WAVE = 64;
@@ -371,6 +373,280 @@ gemm_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
                                                         Out, ldo, ksplit, split, tile, part, counters);
 }
 
+// ------------------------------------------ bf16 MFMA, W streamed (M <= 128)
+// For weight-streaming shapes W is the only large operand and is read once: each
+// wave loads its own WN columns of W from HBM straight into MFMA B-operand
+// registers, D K tiles ahead of use, so W needs no LDS space, no LDS bandwidth
+// and no barrier of its own.  The masked input (NPL planes x BM rows x one K
+// tile, shared by the 4 waves side by side along N) goes global -> LDS by
+// buffer-load-to-LDS (no registers), in the swizzled layout of the tiled kernel,
+// into a ring of D + 1 stages.  Both operands of tile t + D are issued together
+// at tile t: vector-memory loads complete in order, so waiting for an older
+// masked-input tile never waits for a younger W tile.  One barrier per K tile.
+// Split over K, each workgroup writes its partial accumulators in register
+// order (16-byte stores, no atomics) and `stream_sum_kernel` adds the splits in
+// split order and applies the unmask epilogue.
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <int I, int BYTES>
+__device__ __forceinline__ unsigned char* stream_stage()
+{
+    __shared__ __attribute__((aligned(16))) unsigned char buf[BYTES];
+    return buf;
+}
+
+// waits until at most N of this wave's vector-memory operations are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vmem()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+constexpr int ST_NW = 4; // waves per workgroup of the streamed kernel
+
+// v_mfma_f32_32x32x16_bf16 operands: lane l holds row (A) or column (B) l % 32 and
+// k = 8 (l / 32) .. + 7 of a 16-wide k step; result element e of lane l is row
+// 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32.
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// LDS chunk swizzle of the 128-byte masked-input rows: 16-byte chunk c of row r sits
+// in slot c ^ swizzle(r).  SW 0: r & 7; SW 1: (r >> 1) & 7 (pairs of rows share a
+// pattern and differ in the upper half of a 64-bank array).
+template <int SW>
+__device__ __forceinline__ int lds_swizzle(int r)
+{
+    return SW == 0 ? (r & 7) : ((r >> 1) & 7);
+}
+
+template <int NPL, int BM, int WN, int D, int SW = 1>
+__global__ void __launch_bounds__(ST_NW * WAVE)
+gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
+                   const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
+                   float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
+                   int ksplit, int kt_per_split, float* __restrict__ part)
+{
+    constexpr int NW = ST_NW, BN = NW * WN;
+    constexpr int TM = BM / 32, TN = WN / 32; // 32 x 32 MFMA blocks of the wave tile
+    constexpr int S = D + 1;                  // masked-input stages = W register slots
+    constexpr int AROWS = NPL * BM;           // 128-byte LDS rows per stage
+    constexpr int SB = AROWS * 128;
+    constexpr int LA = AROWS / 8 / NW;        // 1 KB LDS-DMA loads per wave per tile
+    constexpr int LW = 4 * TN;                // W loads per wave per tile (4 k steps of 16)
+    static_assert(TM * 32 == BM && TN * 32 == WN, "wave tile");
+    static_assert(AROWS % (8 * NW) == 0, "masked-input stage must split evenly over the waves");
+    static_assert(S >= 2 && S <= 4, "stages");
+    static_assert((D - 1) * (LA + LW) < 64, "loads in flight exceed the wait counter");
+
+    const int tid = threadIdx.x, lane = tid % WAVE;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int tiles = mtiles * ntiles;
+    const int split = (int)lb / tiles, tile = (int)lb % tiles;
+    const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
+    const int ktiles = (K + BK - 1) / BK;
+    const int kt0 = split * kt_per_split;
+    const int kt1 = min(kt0 + kt_per_split, ktiles);
+    const int nk = kt1 > kt0 ? kt1 - kt0 : 0;
+    const int nloop = (nk + S - 1) / S * S; // whole turns of the ring; tiles past kt1 read zeros
+
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
+
+    // masked input: DMA load t of this wave fills 1 KB = stage rows 8j..8j+7 (j = wave + NW t);
+    // lane l writes unit 64j + l: row u / 8, slot u % 8 holding k chunk slot ^ (row & 7)
+    uint32_t aoff[LA];
+    int akc[LA];
+#pragma unroll
+    for (int t = 0; t < LA; ++t) {
+        const int u = (wave + NW * t) * WAVE + lane;
+        const int row = u >> 3, kc = (u & 7) ^ lds_swizzle<SW>(row);
+        const int p = row / BM, r = row - p * BM, gm = m0 + r;
+        akc[t] = kc * 8;
+        aoff[t] = gm < M ? (uint32_t)((p * pstride + (int64_t)gm * lda) * 2 + kc * 16) : OOB;
+    }
+    // W: lane (c = l % 32, h = l / 32) loads row n0 + WN wave + 32 j + c, 16 bytes at k = 16 s + 8 h
+    const int fc = lane % 32, fh = lane / 32;
+    uint32_t woff[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int gn = n0 + wave * WN + j * 32 + fc;
+        woff[j] = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fh * 16) : OOB;
+    }
+
+    unsigned char* const st0 = stream_stage<0, SB>();
+    unsigned char* const st1 = stream_stage<1, SB>();
+    unsigned char* const st2 = S > 2 ? stream_stage<2, SB>() : st0;
+    unsigned char* const st3 = S > 3 ? stream_stage<3, SB>() : st0;
+    auto stage = [&](auto sc) -> unsigned char* {
+        constexpr int q = decltype(sc)::value;
+        return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3;
+    };
+
+    uint4 wb[S][TN][4];
+    // part `part` (0..3) of the loads of relative tile t into ring slot q: W of k step
+    // `part` and a quarter of the masked-input DMA (the remainder with the last part)
+    constexpr int LA4 = LA / 4;
+    auto issue_part = [&](int t, auto sc, int part) {
+        constexpr int q = decltype(sc)::value;
+        const int kt = kt0 + t, kb = kt * BK;
+        const bool live = kt < kt1;
+        unsigned char* sb = stage(sc);
+        const int i0 = part * LA4, i1 = part == 3 ? LA : i0 + LA4;
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            if (i < i0 || i >= i1) continue;
+            const uint32_t off = (live && aoff[i] != OOB && kb + akc[i] < K) ? aoff[i] + (uint32_t)kb * 2 : OOB;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(sb + (wave + NW * i) * 1024), 16, (int)off, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const bool ok = live && woff[j] != OOB && kb + 16 * part + 8 * fh < K;
+            wb[q][j][part] = load16(rw, ok ? woff[j] + (uint32_t)(kb + 16 * part) * 2 : OOB);
+        }
+    };
+    auto issue = [&](int t, auto sc) {
+#pragma unroll
+        for (int part = 0; part < 4; ++part) issue_part(t, sc, part);
+    };
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+    // fragments of k step s: every row block i and plane p
+    auto read_a = [&](const unsigned char* sb, int s, bf16x8_t (&a)[NPL][TM]) {
+        const int kc = s * 2 + fh;
+#pragma unroll
+        for (int p = 0; p < NPL; ++p)
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = p * BM + i * 32 + fc;
+                a[p][i] = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ lds_swizzle<SW>(r)) << 4)));
+            }
+    };
+    // k step s + 1's fragments are read while step s is multiplied; the MFMAs of a
+    // step run plane-major so that the TM x TN accumulators are updated round-robin
+    // (consecutive MFMAs on one accumulator would wait for each other's results).
+    // The loads of the tile D ahead (slot nq) are issued a quarter per k step,
+    // interleaved with the MFMAs, so the matrix cores keep working while they issue.
+    auto compute = [&](int t, auto sc, auto nsc) {
+        constexpr int q = decltype(sc)::value;
+        const unsigned char* sb = stage(sc);
+        bf16x8_t a[2][NPL][TM];
+        read_a(sb, 0, a[0]);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (s + 1 < 4) read_a(sb, s + 1, a[(s + 1) & 1]);
+            issue_part(t + D, nsc, s);
+#pragma unroll
+            for (int p = 0; p < NPL; ++p)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][p][i], as_bf16x8(wb[q][j][s]), acc[i][j], 0, 0, 0);
+            // one group: this step's fragment reads first, then MFMAs with the loads in between
+            __builtin_amdgcn_sched_group_barrier(0x100, NPL * TM, 0);
+#pragma unroll
+            for (int g = 0; g < (LA + 3) / 4 + TN; ++g) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, NPL * TM * TN, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    // one K tile in slot q: this wave's loads of the tile are in (the D - 1 younger
+    // tiles may still be in flight), barrier (everyone's are, and slot q - 1 is no
+    // longer read), multiply slot q while refilling slot q - 1 with tile t + D
+    auto step = [&](int t, auto sc) {
+        constexpr int q = decltype(sc)::value;
+        wait_vmem<(D - 1) * (LA + LW)>();
+        __builtin_amdgcn_s_barrier();
+        compute(t, sc, std::integral_constant<int, (q + D) % S>{});
+    };
+
+    issue(0, std::integral_constant<int, 0>{});
+    if constexpr (D > 1) issue(1, std::integral_constant<int, 1>{});
+    if constexpr (D > 2) issue(2, std::integral_constant<int, 2>{});
+    for (int t = 0; t < nloop; t += S) {
+        step(t, std::integral_constant<int, 0>{});
+        step(t + 1, std::integral_constant<int, 1>{});
+        if constexpr (S > 2) step(t + 2, std::integral_constant<int, 2>{});
+        if constexpr (S > 3) step(t + 3, std::integral_constant<int, 3>{});
+    }
+    wait_vmem<0>(); // the ring's last (zero) tiles have landed before the workgroup ends
+
+    if (ksplit == 1) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = n0 + wave * WN + j * 32 + fc;
+                if (col >= N) continue;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = m0 + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
+                    if (row < M) {
+                        float v = acc[i][j][e];
+                        if (C) v = v - C[(int64_t)row * ldc + col];
+                        Out[(int64_t)row * ldo + col] = v;
+                    }
+                }
+            }
+        return;
+    }
+    // partial in register order: float4 c of block (i, j) of lane l at ((i TN + j) 4 + c) 64 + l
+    float4* mp = reinterpret_cast<float4*>(part) + (((int64_t)tile * ksplit + split) * NW + wave) * (TM * TN * 4 * 64);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                mp[((i * TN + j) * 4 + c) * 64 + lane] =
+                    make_float4(acc[i][j][4 * c], acc[i][j][4 * c + 1], acc[i][j][4 * c + 2], acc[i][j][4 * c + 3]);
+}
+
+// Sums the split-K partials of gemm_stream_kernel in split order and applies the
+// unmask epilogue.  Thread u handles one float4 of one wave's partial (the
+// register order the partials were written in): rows 8 c + 4 (l / 32) + 0..3 of
+// block (i, j), column l % 32.
+template <int BM, int WN>
+__global__ void __launch_bounds__(256)
+stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __restrict__ C, int64_t ldc,
+                  float* __restrict__ Out, int64_t ldo, int M, int N, int mtiles, int tiles)
+{
+    constexpr int NW = ST_NW, BN = NW * WN, TM = BM / 32, TN = WN / 32;
+    constexpr int PER_WAVE = TM * TN * 4 * 64; // float4 units
+    const int64_t total = (int64_t)tiles * NW * PER_WAVE;
+    const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (u >= total) return;
+    const int tile = (int)(u / (NW * PER_WAVE));
+    const int rem = (int)(u - (int64_t)tile * NW * PER_WAVE);
+    const int wave = rem / PER_WAVE, e = rem - wave * PER_WAVE;
+    const int lane = e % 64, ijc = e / 64, c = ijc % 4, ij = ijc / 4, i = ij / TN, j = ij % TN;
+    const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
+    const float4* src = reinterpret_cast<const float4*>(part) + (((int64_t)tile * ksplit) * NW + wave) * PER_WAVE + e;
+    f32x4_t sum = __builtin_bit_cast(f32x4_t, src[0]);
+    for (int q = 1; q < ksplit; ++q) sum += __builtin_bit_cast(f32x4_t, src[(int64_t)q * NW * PER_WAVE]);
+    const int col = n0 + wave * WN + j * 32 + lane % 32;
+    if (col >= N) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int row = m0 + i * 32 + 8 * c + 4 * (lane / 32) + r;
+        if (row < M) {
+            float v = sum[r];
+            if (C) v = v - C[(int64_t)row * ldc + col];
+            Out[(int64_t)row * ldo + col] = v;
+        }
+    }
+}
+
 // --------------------------------------------------------------- f32 MFMA
 // v_mfma_f32_16x16x4_f32 takes one k per lane group; four instructions cover a
 // 16-wide k slice whose elements are assigned so that each lane reads one
@@ -673,8 +949,46 @@ struct Plan {
 
 constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 
+// The W-streamed kernel serves bfloat16 operands at 16 < M <= 128 (M <= 16 is the
+// skinny kernel's).  Variants: 10 bf16x3 BM 128, 11 bf16x3 BM 64, 12 bf16 BM 128,
+// 13 bf16 BM 64; tiles are BM x 256.  The K split fills about 256 CUs, keeps at
+// least ST_MIN_KT K tiles per split and at most ST_MAX_KS splits (measured on the
+// Llama-3.2-3B 128-token projections).
+constexpr int ST_BN = 256, ST_MIN_KT = 6, ST_MAX_KS = 12;
+
+bool use_stream(int64_t M, int prec, int w_type)
+{
+    return prec != SPLITEE_PREC_F32 && w_type == SPLITEE_BF16 && M > 16 && M <= 128;
+}
+
+Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, bool allow_split)
+{
+    Plan p{};
+    const bool x3 = prec == SPLITEE_PREC_BF16X3;
+    p.bm = M > 64 ? 128 : 64;
+    p.bn = ST_BN; p.bk = 64;
+    p.variant = (x3 ? 10 : 12) + (p.bm == 64 ? 1 : 0);
+    p.mtiles = (int)((M + p.bm - 1) / p.bm);
+    p.ntiles = (int)((N + p.bn - 1) / p.bn);
+    p.ktiles = (int)((K + p.bk - 1) / p.bk);
+    const int tiles = p.mtiles * p.ntiles;
+    int ks = 1;
+    if (allow_split && p.ktiles > 0) {
+        ks = 256 / tiles;
+        if (ks > p.ktiles / ST_MIN_KT) ks = p.ktiles / ST_MIN_KT;
+        if (ks > ST_MAX_KS) ks = ST_MAX_KS;
+        if (ks < 1) ks = 1;
+    }
+    p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
+    p.ksplit = p.ktiles > 0 ? (p.ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
+    p.counter_bytes = 0; // the partials are summed by a second kernel: no counters
+    p.part_bytes = p.ksplit > 1 ? (size_t)tiles * p.ksplit * p.bm * p.bn * 4 : 0;
+    return p;
+}
+
 Plan plan_tiled(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allow_split)
 {
+    if (use_stream(M, prec, w_type)) return plan_stream(M, N, K, prec, allow_split);
     Plan p{};
     if (prec == SPLITEE_PREC_F32) {
         p.bm = 128; p.bn = 128; p.bk = 32; p.variant = 0;
@@ -779,7 +1093,26 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         const int64_t planes = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
         if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
             return SPLITEE_ERR_UNSUPPORTED;
-        if (prec == SPLITEE_PREC_BF16) {
+        if (p.variant >= 10) {
+            float* pp = reinterpret_cast<float*>(ws);
+#define ST_LAUNCH(NP, BM_, D_) hipLaunchKernelGGL((gemm_stream_kernel<NP, BM_, 64, D_>), grid, dim3(ST_NW * WAVE), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
+            switch (p.variant) {
+            case 10: ST_LAUNCH(3, 128, 2); break;
+            case 11: ST_LAUNCH(3, 64, 3); break;
+            case 12: ST_LAUNCH(1, 128, 2); break;
+            default: ST_LAUNCH(1, 64, 3); break;
+            }
+#undef ST_LAUNCH
+            if (p.ksplit > 1) {
+                const int tiles = p.mtiles * p.ntiles;
+                const int64_t units = (int64_t)tiles * ST_NW * (p.bm / 32) * 2 * 4 * WAVE;
+                const dim3 g2((unsigned)((units + 255) / 256));
+                if (p.bm == 128)
+                    hipLaunchKernelGGL((stream_sum_kernel<128, 64>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
+                else
+                    hipLaunchKernelGGL((stream_sum_kernel<64, 64>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
+            }
+        } else if (prec == SPLITEE_PREC_BF16) {
             if (p.variant == 0)
                 hipLaunchKernelGGL((gemm_bf16_kernel<1, 128, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
             else
