@@ -12,7 +12,9 @@ through 8 distinct weight sets so the 201 MB per layer is streamed from HBM,
 not the 256 MB MALL.  --workload selects the other shapes: the single float32
 projection, the 28-layer Llama stack at 512 tokens, the 36-layer Qwen3-4B stack
 at 1024 tokens, and Qwen3-4B decode steps (M tokens at position 1024 of a
-2048-position correction bank).
+2048-position correction bank).  At decode sizes (M <= 16, bfloat16 modes) a
+layer's masks are drawn by one launch and each projection is one launch that
+forms fl32(X + eta), multiplies and unmasks.
 
 Prints one JSON line.  Fields beyond the common contract: ``roofline`` (the
 GEMM + unmask kernel: each projection group's launches for every layer or
@@ -82,7 +84,12 @@ def workload_spec(WL, name):
 
 class Path:
     """Device buffers of one workload: per layer (or weight set) and projection
-    group, the weights, the precomputed correction rows and the outputs."""
+    group, the weights, the precomputed correction rows and the outputs.
+
+    Prefill-sized M: per projection, noise + mask in one kernel, then the GEMM with
+    the unmask epilogue.  Decode-sized M (the skinny kernel): per layer, one launch
+    draws the masks of all projection groups, then one launch per projection forms
+    fl32(X + eta), multiplies and unmasks."""
 
     def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets):
         self.torch, self.sp = torch, sp
@@ -106,7 +113,11 @@ class Path:
             dt = torch.float32 if prec == sp.SPLITEE_PREC_F32 else torch.int16
             self.Xt.append(torch.empty((planes, M, p.K), dtype=dt, device=dev))
             self.Y.append(torch.empty((M, p.N), dtype=torch.float32, device=dev))
-            self.ws.append(sp.workspace(M, p.N, p.K, prec, dev, gemm_only=True))
+        self.decode = M <= 16 and prec != sp.SPLITEE_PREC_F32
+        for p in self.projs:
+            self.ws.append(sp.workspace(M, p.N, p.K, prec, dev, gemm_only=not self.decode))
+        self.eta = [torch.empty((M, p.K), dtype=torch.float32, device=dev) for p in self.projs] \
+            if self.decode else None
         self.W, self.C, self.sid = [], [], []
         for l in range(nlayers):
             Ws, sids = [], []
@@ -135,17 +146,32 @@ class Path:
         self.correction_ms = (time.perf_counter() - t0) * 1e3 / nlayers * self.layers_per_step
 
     def gemm(self, l, i):
-        """The GEMM + unmask launch of projection group i of layer (or weight set) l."""
+        """The GEMM + unmask launch of projection group i of layer (or weight set) l
+        (decode: mask + GEMM + unmask, on the mask drawn for the layer)."""
         p, M = self.projs[i], self.M
         W, C = self.W[l][i], self.C[l][i]
-        self.sp.splitee_masked_linear_unmask(self.Xt[i], self.prec, p.K, W, self.wt, p.K, C, C.stride(0),
-                                             self.Y[i], p.N, M, p.N, p.K, self.ws[i][0], self.ws[i][1])
+        if self.decode:
+            self.sp.splitee_masked_linear_fused(
+                self.X[i], p.K, W, self.wt, p.K, C, C.stride(0), self.Y[i], p.N, M, p.N, p.K, self.mech,
+                self.delta, self.eps, 0, self.sid[l][i], self.row0, self.eta[i], self.prec,
+                self.ws[i][0], self.ws[i][1])
+        else:
+            self.sp.splitee_masked_linear_unmask(self.Xt[i], self.prec, p.K, W, self.wt, p.K, C,
+                                                 C.stride(0), self.Y[i], p.N, M, p.N, p.K,
+                                                 self.ws[i][0], self.ws[i][1])
 
     def launches(self, s):
-        """All kernels of step s (noise + mask, then GEMM + unmask, per projection)."""
+        """All kernels of step s: noise, mask, GEMM and unmask of every projection."""
         sp, M = self.sp, self.M
         base = (s % self.nsets) * self.layers_per_step
         for l in range(base, base + self.layers_per_step):
+            if self.decode:
+                Ks = [p.K for p in self.projs]
+                sp.splitee_noise_gen_multi(self.eta, Ks, Ks, self.sid[l], M, self.mech, self.delta,
+                                           self.eps, 0, self.row0)
+                for i in range(len(self.projs)):
+                    self.gemm(l, i)
+                continue
             for i, p in enumerate(self.projs):
                 sp.splitee_noise_mask(self.X[i], p.K, self.Xt[i], self.prec, p.K, M, p.K, self.mech,
                                       self.delta, self.eps, 0, self.sid[l][i], self.row0)
@@ -155,9 +181,11 @@ class Path:
         return self.layers_per_step * sum(2.0 * self.M * p.N * p.K for p in self.projs)
 
     def gemm_bytes(self):
-        """Algorithmic bytes of each GEMM + unmask launch: W, float32 X, C and Y."""
+        """Algorithmic bytes of each GEMM + unmask launch: W, float32 X (and, in the
+        decode launch that forms the masked input, float32 eta), C and Y."""
         wb = 4.0 if self.w_dtype == "f32" else 2.0
-        return [wb * p.N * p.K + 4.0 * self.M * p.K + 8.0 * self.M * p.N for p in self.projs]
+        xb = 8.0 if self.decode else 4.0
+        return [wb * p.N * p.K + xb * self.M * p.K + 8.0 * self.M * p.N for p in self.projs]
 
 
 def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
@@ -356,7 +384,9 @@ def main():
     traffic = measured_traffic(args.workload, pname, names)
     roofline.update({"traffic": None if traffic is None else int(sum(traffic.values())),
                      "traffic_per_launch": traffic and {k: int(v) for k, v in traffic.items()},
-                     "kernel": "GEMM + unmask (one launch per projection group)",
+                     "kernel": ("mask + GEMM + unmask (one launch per projection group, on the masks "
+                                "one launch per layer draws)") if path.decode
+                               else "GEMM + unmask (one launch per projection group)",
                      "launch_us": {p.name: round(u, 2) for p, u in zip(path.projs, per_proj_us)},
                      "bytes_per_launch": {p.name: int(b) for p, b in zip(path.projs, gb)},
                      "flops_per_launch": {p.name: int(f) for p, f in zip(path.projs, gflops)},

@@ -112,6 +112,23 @@ int splitee_noise_gen(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech
                       uint64_t row0, void* stream);
 
 /*
+ * Several noise blocks in one launch: block q is what splitee_noise_gen(eta[q],
+ * ld_eta[q], M, K[q], mech, sensitivity, epsilon, seed, stream_id[q], row0, stream)
+ * writes, element for element.  The blocks share M, the mechanism, seed and row0;
+ * each has its own K, leading dimension and stream id.  This is the per-layer
+ * precomputation of the masks (Sec. "Precomputing the Mask and Noise
+ * Correction"): one launch fills the masks of all projections of a layer.
+ *   eta, ld_eta, K, stream_id   host arrays of `count` entries (1 <= count <= 8,
+ *                               count == 0 does nothing); eta[q] a device pointer,
+ *                               16-byte aligned, ld_eta[q] >= K[q], a multiple of 4
+ * Requires K[q] % 4 == 0.  The host arrays are read during the call only.
+ */
+int splitee_noise_gen_multi(float* const* eta, const int64_t* ld_eta, const int64_t* K,
+                            const uint64_t* stream_id, int count, int64_t M, int mech,
+                            double sensitivity, double epsilon, uint64_t seed, uint64_t row0,
+                            void* stream);
+
+/*
  * Mask: Xt = fl32(X + eta) (the vector addition of Sec. "Offloading Linear
  * Operations"), written in precision out_prec:
  *   F32: float32 M x K (ldxt); BF16: one bfloat16 plane; BF16X3: three bfloat16
@@ -177,14 +194,18 @@ size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
 /*
  * Fused mask -> GEMM -> unmask for one projection: Y = fl32(fl(Xt W^T) - C) with
  * Xt = fl32(X + eta), eta generated in-stream from (mech, Delta, eps, seed,
- * stream_id, row0) -- or taken from eta_override when it is not NULL (M x K float32,
- * leading dimension K; tests inject integer masks this way).  C (M x N, ldc) must be the correction of the same
- * mask, e.g. from splitee_correction with the same noise arguments; for a decode
- * step at positions [t, t+M) pass row0 = t and C = bank + t * ldc.
+ * stream_id, row0) -- or taken from eta_override when it is not NULL: a precomputed
+ * mask (splitee_noise_gen / splitee_noise_gen_multi, Sec. "Precomputing the Mask
+ * and Noise Correction"), M x K float32, leading dimension K, 16-byte aligned; the
+ * noise arguments are then only validated.  C (M x N, ldc) must be the correction
+ * of the same mask, e.g. from splitee_correction with the same noise arguments; for
+ * a decode step at positions [t, t+M) pass row0 = t and C = bank + t * ldc.
  * M <= 16 with BF16 or BF16X3 takes the skinny bandwidth-bound kernel (decode);
- * otherwise the tiled MFMA kernel runs, split over K when the tile count is small.  workspace: >= splitee_fused_workspace_bytes(M, N, K, prec)
- * bytes, 256-byte aligned; it must hold zeros before its first use and calls
- * leave it that way.
+ * given eta_override it forms fl32(X + eta) and its bfloat16 planes inside that
+ * kernel (one launch, bit-identical to the two-launch path).  Otherwise the tiled
+ * or W-streamed MFMA kernel runs, split over K when the tile count is small.
+ * workspace: >= splitee_fused_workspace_bytes(M, N, K, prec) bytes, 256-byte
+ * aligned; it must hold zeros before its first use and calls leave it that way.
  */
 int splitee_masked_linear_fused(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
                                 const float* C, int64_t ldc, float* Y, int64_t ldy, int64_t M,

@@ -26,6 +26,7 @@ EXPORTED = [
     "splitee_masked_linear", "splitee_unmask", "splitee_fused_workspace_bytes",
     "splitee_masked_linear_fused", "splitee_correction", "splitee_transform_probe",
     "splitee_noise_mask", "splitee_gemm_workspace_bytes", "splitee_masked_linear_unmask",
+    "splitee_noise_gen_multi",
 ]
 
 
@@ -65,6 +66,7 @@ def load():
         "splitee_gemm_workspace_bytes": (SZ, [I64, I64, I64, I]),
         "splitee_masked_linear_unmask": (I, [P, I, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, P,
                                              SZ, P]),
+        "splitee_noise_gen_multi": (I, [P, P, P, P, I, I64, I, D, D, U64, U64, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -122,6 +124,21 @@ def splitee_noise_gen(eta, ld_eta, M, K, mech, sensitivity, epsilon, seed, strea
                       stream=None):
     _check("splitee_noise_gen", load().splitee_noise_gen(
         _ptr(eta), ld_eta, M, K, mech, sensitivity, epsilon, seed, stream_id, row0, _stream(stream)))
+
+
+def splitee_noise_gen_multi(etas, ld_etas, Ks, stream_ids, M, mech, sensitivity, epsilon, seed,
+                            row0=0, stream=None):
+    """etas, ld_etas, Ks, stream_ids: sequences of equal length (the noise blocks)."""
+    n = len(etas)
+    if not (len(ld_etas) == len(Ks) == len(stream_ids) == n):
+        raise ValueError("splitee_noise_gen_multi: per-block sequences differ in length")
+    ptrs = (ctypes.c_void_p * max(n, 1))(*[_ptr(e) for e in etas])
+    lds = (ctypes.c_int64 * max(n, 1))(*ld_etas)
+    ks = (ctypes.c_int64 * max(n, 1))(*Ks)
+    sids = (ctypes.c_uint64 * max(n, 1))(*stream_ids)
+    _check("splitee_noise_gen_multi", load().splitee_noise_gen_multi(
+        ctypes.cast(ptrs, ctypes.c_void_p), ctypes.cast(lds, ctypes.c_void_p), ctypes.cast(ks, ctypes.c_void_p),
+        ctypes.cast(sids, ctypes.c_void_p), n, M, mech, sensitivity, epsilon, seed, row0, _stream(stream)))
 
 
 def splitee_mask(X, ldx, eta, ld_eta, Xt, out_prec, ldxt, M, K, stream=None):

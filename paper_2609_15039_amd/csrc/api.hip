@@ -94,6 +94,10 @@ int run_masked(const float* X, int64_t ldx, const void* W, int w_type, int64_t l
     if (ws && (reinterpret_cast<uintptr_t>(ws) & 255u)) return SPLITEE_ERR_ALIGN;
     if (M == 0 || N == 0) return SPLITEE_OK;
     char* base = reinterpret_cast<char*>(ws);
+    if (eta_override && use_skinny(M, prec))
+        // decode with a precomputed mask: the GEMM forms fl32(X + eta) itself
+        return splitee_host::launch_skinny_masked(X, ldx, eta_override, K, prec, W, ldw, C, ldc, Y, ldy, M, N,
+                                                  K, base, gws, s);
     void* Xt = base + gws;
     unsigned* counters = reinterpret_cast<unsigned*>(base);
     const int64_t ncounters = (int64_t)(gemm_counters(M, N, K, prec, w_type) / 4);
@@ -137,6 +141,26 @@ int splitee_noise_gen(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech
     if (!aligned16(eta) || !pitch16(ld_eta, 4)) return SPLITEE_ERR_ALIGN;
     return splitee_host::launch_noise(eta, ld_eta, M, K, mech, sensitivity / epsilon, seed, stream_id,
                                       row0, as_stream(stream));
+}
+
+int splitee_noise_gen_multi(float* const* eta, const int64_t* ld_eta, const int64_t* K,
+                            const uint64_t* stream_id, int count, int64_t M, int mech, double sensitivity,
+                            double epsilon, uint64_t seed, uint64_t row0, void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (count < 0 || count > splitee::NOISE_MULTI_MAX) return SPLITEE_ERR_ARG;
+    if (count == 0) return SPLITEE_OK;
+    if (!eta || !ld_eta || !K || !stream_id) return SPLITEE_ERR_ARG;
+    if (!dims_ok(M, 0, 0)) return SPLITEE_ERR_SHAPE;
+    for (int q = 0; q < count; ++q) {
+        if (!dims_ok(M, 0, K[q]) || K[q] % 4 != 0 || ld_eta[q] < K[q]) return SPLITEE_ERR_SHAPE;
+        if (M > 0 && K[q] > 0 && !eta[q]) return SPLITEE_ERR_ARG;
+        if (eta[q] && (!aligned16(eta[q]) || !pitch16(ld_eta[q], 4))) return SPLITEE_ERR_ALIGN;
+    }
+    if (M == 0) return SPLITEE_OK;
+    return splitee_host::launch_noise_multi(eta, ld_eta, K, stream_id, count, M, mech, sensitivity / epsilon,
+                                            seed, row0, as_stream(stream));
 }
 
 int splitee_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, void* Xt,

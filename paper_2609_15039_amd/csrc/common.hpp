@@ -11,6 +11,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 namespace splitee {
 
+// most noise blocks one splitee_noise_gen_multi call generates
+constexpr int NOISE_MULTI_MAX = 8;
+
 // binary32 -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
 __device__ __forceinline__ uint32_t bf16_bits_rne(float x)
 {
@@ -49,6 +52,8 @@ __device__ __forceinline__ uint32_t xcd_logical_block(uint32_t b, uint32_t nbloc
 namespace splitee_host {
 int launch_noise(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech, double scale,
                  uint64_t seed, uint64_t sid, uint64_t row0, hipStream_t s);
+int launch_noise_multi(float* const* eta, const int64_t* ld, const int64_t* K, const uint64_t* sid, int count,
+                       int64_t M, int mech, double scale, uint64_t seed, uint64_t row0, hipStream_t s);
 int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int gen_mech,
                 double scale, uint64_t seed, uint64_t sid, uint64_t row0, void* Xt, int prec,
                 int64_t ldxt, int64_t plane_stride, int64_t M, int64_t K,
@@ -62,6 +67,11 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_typ
 int launch_gemm(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
                 int w_type, int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo,
                 int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+// Decode GEMM whose masked input fl32(X + eta) is formed in-kernel from X and a
+// given mask eta (both M x K float32).
+int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec,
+                         const void* W, int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo,
+                         int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
 size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
 int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
                   int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,

@@ -409,8 +409,6 @@ constexpr int ST_NW = 4; // waves per workgroup of the streamed kernel
 // v_mfma_f32_32x32x16_bf16 operands: lane l holds row (A) or column (B) l % 32 and
 // k = 8 (l / 32) .. + 7 of a 16-wide k step; result element e of lane l is row
 // 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32.
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
 // LDS chunk swizzle of the 128-byte masked-input rows: 16-byte chunk c of row r sits
 // in slot c ^ swizzle(r).  SW 0: r & 7; SW 1: (r >> 1) & 7 (pairs of rows share a
 // pattern and differ in the upper half of a 64-bank array).
@@ -804,10 +802,39 @@ constexpr int SK_LDS_MAX = 64 * 1024; // masked-input slice per workgroup (two w
 constexpr int SK_TARGET_WGS = 512;
 constexpr int SK_CP = SK_LDS_MAX / 16 / 256; // slice units per thread (16 at 64 KB)
 
-template <int NPL, int R>
+// Where the skinny kernel's masked input comes from: NPL bfloat16 planes A
+// (plane p at A + p * pstride), or (MASK) float32 X and mask eta, from which the
+// kernel forms fl32(X + eta) and its planes itself.
+struct SkSrc {
+    const uint16_t* A; int64_t lda, pstride;
+    const float* X; int64_t ldx;
+    const float* eta; int64_t ld_eta;
+};
+
+constexpr int SK_MCP = 2; // masked-input units (8 float32 of X and of eta) per thread per load round
+
+template <int NPL>
+__device__ __forceinline__ void planes_of(const float (&x)[8], uint4 (&q)[NPL])
+{
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        if (NPL == 1) {
+            reinterpret_cast<uint32_t*>(&q[0])[h] =
+                splitee::bf16_bits_rne(x[2 * h]) | (splitee::bf16_bits_rne(x[2 * h + 1]) << 16);
+        } else {
+            uint32_t h0, m0, l0, h1, m1, l1;
+            splitee::split3_bf16(x[2 * h], h0, m0, l0);
+            splitee::split3_bf16(x[2 * h + 1], h1, m1, l1);
+            reinterpret_cast<uint32_t*>(&q[0])[h] = h0 | (h1 << 16);
+            reinterpret_cast<uint32_t*>(&q[1])[h] = m0 | (m1 << 16);
+            reinterpret_cast<uint32_t*>(&q[2])[h] = l0 | (l1 << 16);
+        }
+    }
+}
+
+template <int NPL, int R, bool MASK>
 __global__ void __launch_bounds__(256)
-skinny_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
-              const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
+skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
               float* __restrict__ Out, int64_t ldo, int M, int N, int K, int ntiles, int ksplit,
               int steps_per_split, float* __restrict__ part, unsigned* __restrict__ counters)
 {
@@ -824,24 +851,7 @@ skinny_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     const int RS = SA * 64 + 16;                      // LDS row pitch; 16 bytes of padding
     const int fr = lane % 16, fq = lane / 16;
 
-    // 1. slice loads: plane p, row r < M, 16-byte unit c of the row's SA * 64 bytes
-    const int upr = SA * 4, units = NPL * M * upr;
-    uint4 av[SK_CP];
-    {
-        const __amdgpu_buffer_rsrc_t ra =
-            make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
-#pragma unroll
-        for (int i = 0; i < SK_CP; ++i) {
-            const int u = i * 256 + tid;
-            const int pr = u / upr, c = u - pr * upr;
-            const int p = pr / M, r = pr - p * M;
-            const int k = s0 * 32 + c * 8;
-            const bool ok = u < units && c < ns * 4 && k < K;
-            av[i] = load16(ra, ok ? (uint32_t)((p * pstride + (int64_t)r * lda + k) * 2) : OOB);
-        }
-    }
-
-    // 2. the W ring
+    // the W ring
     const int gn = n0 + wave * 16 + fr;
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
     const uint32_t wbase = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fq * 16) : OOB;
@@ -850,16 +860,94 @@ skinny_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
         return load16(rw, ok ? wbase + (uint32_t)(s0 + j) * 64 : OOB);
     };
     uint4 ring[R];
-#pragma unroll
-    for (int u = 0; u < R; ++u) ring[u] = wload(u);
 
-    // 3. slice to LDS (waits for the slice loads only: loads complete in order)
+    if constexpr (!MASK) {
+        // 1. slice loads: plane p, row r < M, 16-byte unit c of the row's SA * 64 bytes
+        const int upr = SA * 4, units = NPL * M * upr;
+        uint4 av[SK_CP];
+        const __amdgpu_buffer_rsrc_t ra =
+            make_rsrc(src.A, (uint32_t)((NPL - 1) * src.pstride * 2 + (int64_t)M * src.lda * 2));
 #pragma unroll
-    for (int i = 0; i < SK_CP; ++i) {
-        const int u = i * 256 + tid;
-        if (u < units) {
+        for (int i = 0; i < SK_CP; ++i) {
+            const int u = i * 256 + tid;
             const int pr = u / upr, c = u - pr * upr;
-            *reinterpret_cast<uint4*>(sa + pr * RS + c * 16) = av[i];
+            const int p = pr / M, r = pr - p * M;
+            const int k = s0 * 32 + c * 8;
+            const bool ok = u < units && c < ns * 4 && k < K;
+            av[i] = load16(ra, ok ? (uint32_t)((p * src.pstride + (int64_t)r * src.lda + k) * 2) : OOB);
+        }
+        // 2. the ring, queued behind the slice
+#pragma unroll
+        for (int u = 0; u < R; ++u) ring[u] = wload(u);
+        // 3. slice to LDS (waits for the slice loads only: loads complete in order)
+#pragma unroll
+        for (int i = 0; i < SK_CP; ++i) {
+            const int u = i * 256 + tid;
+            if (u < units) {
+                const int pr = u / upr, c = u - pr * upr;
+                *reinterpret_cast<uint4*>(sa + pr * RS + c * 16) = av[i];
+            }
+        }
+    } else {
+        // 1-3 with the mask formed here: unit c of row r is 8 float32 of X and of
+        // eta at k = s0 * 32 + 8 c; the unit's fl32(X + eta) is split into the NPL
+        // planes and stored where the plane form would have put it.  The first
+        // round's loads go out before the ring, the rest after it.
+        const int upr = SA * 4, units = M * upr;
+        const __amdgpu_buffer_rsrc_t rx = make_rsrc(src.X, (uint32_t)((int64_t)M * src.ldx * 4));
+        const __amdgpu_buffer_rsrc_t re = make_rsrc(src.eta, (uint32_t)((int64_t)M * src.ld_eta * 4));
+        auto unit_ok = [&](int u, int& r, int& c, int& k) {
+            r = u / upr;
+            c = u - r * upr;
+            k = s0 * 32 + c * 8;
+            return u < units && c < ns * 4 && k < K;
+        };
+        auto round_load = [&](int base, uint4 (&xv)[SK_MCP][2], uint4 (&ev)[SK_MCP][2]) {
+#pragma unroll
+            for (int i = 0; i < SK_MCP; ++i) {
+                int r, c, k;
+                const bool ok = unit_ok(base + i * 256 + tid, r, c, k);
+                const uint32_t ox = ok ? (uint32_t)(((int64_t)r * src.ldx + k) * 4) : OOB;
+                const uint32_t oe = ok ? (uint32_t)(((int64_t)r * src.ld_eta + k) * 4) : OOB;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    ev[i][h] = load16(re, oe == OOB ? OOB : oe + 16 * h);
+                    xv[i][h] = load16(rx, ox == OOB ? OOB : ox + 16 * h);
+                }
+            }
+        };
+        auto round_store = [&](int base, const uint4 (&xv)[SK_MCP][2], const uint4 (&ev)[SK_MCP][2]) {
+#pragma unroll
+            for (int i = 0; i < SK_MCP; ++i) {
+                const int u = base + i * 256 + tid;
+                if (u < units) {
+                    const int r = u / upr, c = u - r * upr;
+                    float x[8];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const float4 e = __builtin_bit_cast(float4, ev[i][h]);
+                        const float4 v = __builtin_bit_cast(float4, xv[i][h]);
+                        x[4 * h + 0] = v.x + e.x;
+                        x[4 * h + 1] = v.y + e.y;
+                        x[4 * h + 2] = v.z + e.z;
+                        x[4 * h + 3] = v.w + e.w;
+                    }
+                    uint4 q[NPL];
+                    planes_of<NPL>(x, q);
+#pragma unroll
+                    for (int p = 0; p < NPL; ++p)
+                        *reinterpret_cast<uint4*>(sa + (p * M + r) * RS + c * 16) = q[p];
+                }
+            }
+        };
+        uint4 xv[SK_MCP][2], ev[SK_MCP][2];
+        round_load(0, xv, ev);
+#pragma unroll
+        for (int u = 0; u < R; ++u) ring[u] = wload(u);
+        round_store(0, xv, ev);
+        for (int base = SK_MCP * 256; base < units; base += SK_MCP * 256) {
+            round_load(base, xv, ev);
+            round_store(base, xv, ev);
         }
     }
     __syncthreads();
@@ -1151,12 +1239,40 @@ int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const v
     unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
     float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
     dim3 grid((unsigned)(p.ntiles * p.ksplit));
-    const uint16_t* a = reinterpret_cast<const uint16_t*>(A);
+    const SkSrc src{reinterpret_cast<const uint16_t*>(A), lda, pstride, nullptr, 0, nullptr, 0};
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
     if (prec == SPLITEE_PREC_BF16)
-        hipLaunchKernelGGL((skinny_kernel<1, SK_RING>), grid, dim3(256), lds, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        hipLaunchKernelGGL((skinny_kernel<1, SK_RING, false>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
     else
-        hipLaunchKernelGGL((skinny_kernel<3, SK_RING>), grid, dim3(256), lds, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        hipLaunchKernelGGL((skinny_kernel<3, SK_RING, false>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
+
+int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec,
+                         const void* W, int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo,
+                         int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (M > 16 || prec == SPLITEE_PREC_F32) return SPLITEE_ERR_UNSUPPORTED;
+    if (!X || !eta) return SPLITEE_ERR_ARG;
+    if (K % 8 != 0 || ld_eta < K || ldx < K) return SPLITEE_ERR_SHAPE;
+    if (M * ld_eta * 4 >= (int64_t(1) << 31) || M * ldx * 4 >= (int64_t(1) << 31) ||
+        N * ldw * 2 >= (int64_t(1) << 31))
+        return SPLITEE_ERR_UNSUPPORTED;
+    const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
+    Plan p = plan_skinny(M, N, K, prec);
+    const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
+    if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
+    if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
+    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
+    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
+    dim3 grid((unsigned)(p.ntiles * p.ksplit));
+    const SkSrc src{nullptr, 0, 0, X, ldx, eta, ld_eta};
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+    if (prec == SPLITEE_PREC_BF16)
+        hipLaunchKernelGGL((skinny_kernel<1, SK_RING, true>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+    else
+        hipLaunchKernelGGL((skinny_kernel<3, SK_RING, true>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 

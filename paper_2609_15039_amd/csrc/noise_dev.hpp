@@ -1,0 +1,278 @@
+// Device-side noise stream of the masked linear layer (gfx950): Philox4x32-10
+// words and the correctly rounded binary32 transforms (Laplace inverse CDF,
+// Box-Muller radius and angle) scaled by Delta / eps.  The noise law is Prop. 2
+// (Gaussian, std Delta/eps) or Laplace of scale Delta/eps; the generator and the
+// rounding are the library's definition given in include/splitee.h.  Every
+// transform value is the correctly rounded binary32 value of the real function:
+// it is evaluated in binary64 and kept when the binary64 value is on the right
+// side of every binary32 rounding boundary by more than a relative error budget
+// of 2^-48 (at least 16 binary64 ulps, above the error of the device library's
+// log / sqrt / sincospi), and otherwise recomputed in double-double arithmetic
+// (about 100 correct bits) -- Ziv's strategy.  Included by the noise / mask
+// kernels and by the decode GEMM, which generates its masked-input slice itself.
+#pragma once
+#include "common.hpp"
+#include <math.h>
+
+#pragma clang fp contract(off)
+
+namespace {  // internal to each translation unit that includes this header
+
+// ------------------------------------------------------------- Philox4x32-10
+// Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11.
+struct u32x4 { uint32_t x, y, z, w; };
+
+__device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+        uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+        c = u32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return c;
+}
+
+// --------------------------------------------------- double-double arithmetic
+// Dekker (1971) / Knuth error-free transformations; fma gives the exact product
+// error.  Contraction is off in this file so every other operation is one IEEE
+// binary64 rounding.
+struct dd { double hi, lo; };
+
+__device__ __forceinline__ dd two_sum(double a, double b)
+{
+    double s = a + b, bb = s - a;
+    return dd{s, (a - (s - bb)) + (b - bb)};
+}
+__device__ __forceinline__ dd fast_two_sum(double a, double b)
+{
+    double s = a + b;
+    return dd{s, b - (s - a)};
+}
+__device__ __forceinline__ dd two_prod(double a, double b)
+{
+    double p = a * b;
+    return dd{p, __builtin_fma(a, b, -p)};
+}
+__device__ __forceinline__ dd dd_add(dd x, dd y)
+{
+    dd s = two_sum(x.hi, y.hi), t = two_sum(x.lo, y.lo);
+    s.lo += t.hi;
+    s = fast_two_sum(s.hi, s.lo);
+    s.lo += t.lo;
+    return fast_two_sum(s.hi, s.lo);
+}
+__device__ __forceinline__ dd dd_neg(dd x) { return dd{-x.hi, -x.lo}; }
+__device__ __forceinline__ dd dd_mul(dd x, dd y)
+{
+    dd p = two_prod(x.hi, y.hi);
+    p.lo += x.hi * y.lo + x.lo * y.hi;
+    return fast_two_sum(p.hi, p.lo);
+}
+__device__ __forceinline__ dd dd_mul_d(dd x, double y)
+{
+    dd p = two_prod(x.hi, y);
+    p.lo += x.lo * y;
+    return fast_two_sum(p.hi, p.lo);
+}
+__device__ __forceinline__ dd dd_div(dd a, dd b)
+{
+    double q1 = a.hi / b.hi;
+    dd r = dd_add(a, dd_neg(dd_mul_d(b, q1)));
+    double q2 = r.hi / b.hi;
+    r = dd_add(r, dd_neg(dd_mul_d(b, q2)));
+    double q3 = r.hi / b.hi;
+    dd q = fast_two_sum(q1, q2);
+    return dd_add(q, dd{q3, 0.0});
+}
+__device__ __forceinline__ dd dd_div_d(dd a, double b) { return dd_div(a, dd{b, 0.0}); }
+
+// ln 2 and 2 pi as double-double (each pair within 1e-32 relative of the constant)
+#define DD_LN2_HI 0x1.62e42fefa39efp-1
+#define DD_LN2_LO 0x1.abc9e3b39803fp-56
+#define DD_2PI_HI 0x1.921fb54442d18p+2
+#define DD_2PI_LO 0x1.1a62633145c07p-52
+
+// ln x for a positive normal binary64 x.  x = m 2^e with m in [sqrt(1/2), sqrt(2)),
+// ln m = 2 atanh(s), s = (m - 1)/(m + 1), |s| < 0.172, and
+// atanh(s)/s = sum_k s^(2k) / (2k + 1), 25 terms (s^50 < 2^-127).
+__device__ __attribute__((noinline)) dd dd_log(double x)
+{
+    int e;
+    double m = frexp(x, &e); // m in [1/2, 1)
+    if (m < 0.70710678118654752440) {
+        m *= 2.0;
+        e -= 1;
+    }
+    dd num = two_sum(m, -1.0), den = two_sum(m, 1.0);
+    dd s = dd_div(num, den);
+    dd z = dd_mul(s, s);
+    const int NT = 25;
+    dd acc = dd_div_d(dd{1.0, 0.0}, (double)(2 * NT + 1));
+    for (int k = NT - 1; k >= 0; --k)
+        acc = dd_add(dd_mul(acc, z), dd_div_d(dd{1.0, 0.0}, (double)(2 * k + 1)));
+    dd lnm = dd_mul_d(dd_mul(s, acc), 2.0);
+    dd eln2 = dd_add(two_prod((double)e, DD_LN2_HI), dd{(double)e * DD_LN2_LO, 0.0});
+    return dd_add(eln2, lnm);
+}
+
+__device__ dd dd_sqrt(dd v)
+{
+    double r = sqrt(v.hi);
+    dd r2 = two_prod(r, r);
+    double corr = ((v.hi - r2.hi) - r2.lo + v.lo) / (2.0 * r);
+    return fast_two_sum(r, corr);
+}
+
+// sin and cos of g = 2 pi f for exact f in [0, 1/8], Taylor series to degree 31.
+__device__ void dd_sincos_2pi_small(double f, dd& sn, dd& cs)
+{
+    dd g = dd_add(two_prod(DD_2PI_HI, f), dd{DD_2PI_LO * f, 0.0});
+    dd g2 = dd_mul(g, g);
+    dd ts = g, ssum = g, tc = dd{1.0, 0.0}, csum = dd{1.0, 0.0};
+    for (int n = 1; n <= 15; ++n) {
+        ts = dd_div_d(dd_mul(ts, g2), (double)((2 * n) * (2 * n + 1)));
+        tc = dd_div_d(dd_mul(tc, g2), (double)((2 * n - 1) * (2 * n)));
+        if (n & 1) {
+            ssum = dd_add(ssum, dd_neg(ts));
+            csum = dd_add(csum, dd_neg(tc));
+        } else {
+            ssum = dd_add(ssum, ts);
+            csum = dd_add(csum, tc);
+        }
+    }
+    sn = ssum;
+    cs = csum;
+}
+
+// sin and cos of 2 pi u(w) in double-double: octant reduction of the exact
+// u = j / 2^33 (j = 2w + 1), then the series on an argument in [0, pi/4].
+__device__ __attribute__((noinline)) void dd_sincos_2pi(uint32_t w, dd& sn, dd& cs)
+{
+    uint64_t j = 2ull * (uint64_t)w + 1ull;
+    int oct = (int)(j >> 30);
+    uint64_t jf = j - ((uint64_t)oct << 30);
+    double f = (double)jf * 0x1p-33;                     // u - oct/8
+    double h = (double)((1ull << 30) - jf) * 0x1p-33;    // (oct+1)/8 - u
+    // angle within the octant measured from its nearer axis: even octants from
+    // the start (f), odd octants from the end (h)
+    dd s1, c1;
+    dd_sincos_2pi_small((oct & 1) ? h : f, s1, c1);
+    dd s, c;
+    switch (oct) {
+    case 0: s = s1;         c = c1;         break;
+    case 1: s = c1;         c = s1;         break;
+    case 2: s = c1;         c = dd_neg(s1); break;
+    case 3: s = s1;         c = dd_neg(c1); break;
+    case 4: s = dd_neg(s1); c = dd_neg(c1); break;
+    case 5: s = dd_neg(c1); c = dd_neg(s1); break;
+    case 6: s = dd_neg(c1); c = s1;         break;
+    default: s = dd_neg(s1); c = c1;        break;
+    }
+    sn = s;
+    cs = c;
+}
+
+// --------------------------------------------------- rounding to binary32
+
+// Neighbour of nonzero finite binary32 f in the direction of `up` (toward +inf if up).
+__device__ __forceinline__ float f32_step(float f, bool up)
+{
+    uint32_t b = __float_as_uint(f);
+    bool mag_up = (up == (f > 0.0f));
+    return __uint_as_float(mag_up ? b + 1u : b - 1u);
+}
+
+// RN32 of a double-double value (hi + lo, |lo| <= ulp(hi)/2).  Only when hi is
+// exactly a binary32 midpoint can lo change the result.
+__device__ __forceinline__ float round_dd_f32(dd v)
+{
+    float f = (float)v.hi;
+    double fd = (double)f;
+    if (v.hi != fd && v.lo != 0.0) {
+        float g = f32_step(f, v.hi > fd);
+        double mid = 0.5 * (fd + (double)g);
+        if (v.hi == mid) {
+            bool toward_g = (g > f) ? (v.lo > 0.0) : (v.lo < 0.0);
+            return toward_g ? g : f;
+        }
+    }
+    return f;
+}
+
+// RN32(r) is the correctly rounded value of the real function whenever the true
+// value lies within |r| 2^-48 of r and no binary32 midpoint lies that close to r.
+__device__ __forceinline__ bool round_f32_safe(double r, float& out)
+{
+    float f = (float)r;
+    double fd = (double)f;
+    double m_up = 0.5 * (fd + (double)f32_step(f, true));
+    double m_dn = 0.5 * (fd + (double)f32_step(f, false));
+    double d = fmin(fabs(r - m_up), fabs(r - m_dn));
+    out = f;
+    return d > fabs(r) * 0x1p-48;
+}
+
+// ---------------------------------------------------- the four transforms
+
+__device__ __forceinline__ float cr_laplace_t(uint32_t w, bool force_slow)
+{
+    const bool upper = w >= 0x80000000u;
+    // 2u = (2w + 1) 2^-32 and 2 - 2u = (2^33 - 2w - 1) 2^-32, both exact
+    const uint64_t j = upper ? ((1ull << 33) - 2ull * (uint64_t)w - 1ull) : (2ull * (uint64_t)w + 1ull);
+    const double x = (double)j * 0x1p-32;
+    float f;
+    if (force_slow || !round_f32_safe(log(x), f)) f = round_dd_f32(dd_log(x));
+    return upper ? -f : f;
+}
+
+__device__ __forceinline__ float cr_gauss_r(uint32_t w, bool force_slow)
+{
+    const double u = ((double)w + 0.5) * 0x1p-32;
+    float f;
+    if (force_slow || !round_f32_safe(sqrt(-2.0 * log(u)), f))
+        f = round_dd_f32(dd_sqrt(dd_mul_d(dd_log(u), -2.0)));
+    return f;
+}
+
+__device__ __forceinline__ void cr_sincos_2pi(uint32_t w, bool force_slow, float& sn, float& cs)
+{
+    const double x = (double)(2ull * (uint64_t)w + 1ull) * 0x1p-32; // 2u, exact
+    double s64, c64;
+    sincospi(x, &s64, &c64);
+    bool ok_s = !force_slow && round_f32_safe(s64, sn);
+    bool ok_c = !force_slow && round_f32_safe(c64, cs);
+    if (!(ok_s && ok_c)) {
+        dd s, c;
+        dd_sincos_2pi(w, s, c);
+        if (!ok_s) sn = round_dd_f32(s);
+        if (!ok_c) cs = round_dd_f32(c);
+    }
+}
+
+// eta for one pair of consecutive elements of a row: lanes (0,1) or (2,3) of
+// Philox block b (half = 0 or 1).
+__device__ __forceinline__ float2 noise_pair(int mech, double scale, uint64_t b, int half,
+                                             uint32_t sid_lo, uint32_t sid_hi, uint32_t k0, uint32_t k1)
+{
+    if (mech == SPLITEE_MECH_NONE) return make_float2(0.f, 0.f);
+    u32x4 w = philox4x32_10(u32x4{(uint32_t)b, (uint32_t)(b >> 32), sid_lo, sid_hi}, k0, k1);
+    const uint32_t wa = half ? w.z : w.x, wb = half ? w.w : w.y;
+    float2 o;
+    if (mech == SPLITEE_MECH_LAPLACE) {
+        o.x = (float)(scale * (double)cr_laplace_t(wa, false));
+        o.y = (float)(scale * (double)cr_laplace_t(wb, false));
+    } else {
+        const float r = cr_gauss_r(wa, false);
+        float sn, cs;
+        cr_sincos_2pi(wb, false, sn, cs);
+        // r * c is exact in binary64 (24 + 24 significant bits)
+        o.x = (float)(scale * ((double)r * (double)cs));
+        o.y = (float)(scale * ((double)r * (double)sn));
+    }
+    return o;
+}
+
+}  // namespace

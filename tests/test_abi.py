@@ -61,6 +61,27 @@ def test_noise_gen_validation(lib, kw, code):
     assert noise(lib, **kw) == code
 
 
+def noise_multi(lib, etas=(P, P), lds=(8, 16), ks=(8, 16), sids=(0, 1), count=None, M=2, mech=G,
+                d=1.0, e=1.0, null_arrays=False):
+    n = len(etas)
+    arr = lambda t, v: (t * max(n, 1))(*v)
+    a = [arr(ctypes.c_void_p, etas), arr(ctypes.c_int64, lds), arr(ctypes.c_int64, ks),
+         arr(ctypes.c_uint64, sids)]
+    a = [None if null_arrays else ctypes.cast(x, ctypes.c_void_p) for x in a]
+    return lib.splitee_noise_gen_multi(*a, n if count is None else count, M, mech, d, e, 0, 0, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(e=0.0), ARG), (dict(d=math.inf), ARG), (dict(mech=5), ARG),
+    (dict(count=9), ARG), (dict(count=-1), ARG), (dict(null_arrays=True), ARG),
+    (dict(ks=(8, 6)), SHAPE), (dict(lds=(8, 12)), SHAPE), (dict(M=-3), SHAPE),
+    (dict(etas=(P, 8)), ALIGN), (dict(lds=(8, 18)), ALIGN), (dict(etas=(P, None)), ARG),
+    (dict(count=0, null_arrays=True), OK), (dict(M=0), OK),
+    (dict(etas=(None, None), ks=(0, 0), lds=(0, 0)), OK)])
+def test_noise_gen_multi_validation(lib, kw, code):
+    assert noise_multi(lib, **kw) == code
+
+
 def test_mask_validation(lib):
     f = lib.splitee_mask
     assert f(P, 8, P, 8, P, 7, 8, 2, 8, None) == UNSUP

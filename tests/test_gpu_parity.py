@@ -101,6 +101,32 @@ def test_noise_rows_are_bank_rows():
     assert torch.equal(bank[t:t + M].view(torch.int32), step.view(torch.int32))
 
 
+@pytest.mark.parametrize("mech", ["laplace", "gaussian", "none"])
+def test_noise_gen_multi_bit_exact(mech):
+    # the blocks of one launch are the single-block noise, element for element
+    g, o = MECH[mech]
+    M, row0, seed = 7, 123, 2**40 + 9
+    Ks = (3072, 264, 8192, 8)
+    lds = (3072, 272, 8200, 12)
+    sids = (WL.stream_id(1, 0), WL.stream_id(1, 1), 99, 2**50 + 3)
+    etas = [torch.full((M, ld), float("nan"), device=DEV) for ld in lds]
+    sp.splitee_noise_gen_multi(etas, lds, Ks, sids, M, g, 825.27, 2.0, seed, row0)
+    for eta, K, sid in zip(etas, Ks, sids):
+        got = host(eta)
+        assert np.array_equal(bits(got[:, :K]), bits(O.noise(M, K, o, 825.27, 2.0, seed, sid, row0)))
+        assert np.all(np.isnan(got[:, K:]))
+
+
+def test_noise_gen_multi_eight_blocks_equal_single_calls():
+    M, K = 16, 2560
+    sids = [WL.stream_id(5, q) for q in range(8)]
+    etas = [torch.empty((M, K), device=DEV) for _ in sids]
+    sp.splitee_noise_gen_multi(etas, [K] * 8, [K] * 8, sids, M, sp.SPLITEE_MECH_GAUSSIAN, 719.8, 2.0, 4, 1000)
+    for eta, sid in zip(etas, sids):
+        one = sp.noise(M, K, sp.SPLITEE_MECH_GAUSSIAN, 719.8, 2.0, 4, sid, row0=1000)
+        assert torch.equal(eta.view(torch.int32), one.view(torch.int32))
+
+
 # ------------------------------------------------------------------------- mask
 
 @pytest.mark.parametrize("prec", ["f32", "bf16", "bf16x3"])
@@ -209,6 +235,33 @@ def test_fused_within_theorem4_gate(prec, mech, M, N, K, delta, eps):
 def test_fused_skinny_decode(prec, M, N, K):
     err, b, _, _ = _fused_case(M, N, K, "gaussian", 719.8, 2.0, prec, row0=1000 + M)
     assert np.all(err <= b["gate"])
+
+
+@pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
+@pytest.mark.parametrize("M", [1, 3, 16])
+@pytest.mark.parametrize("N,K,xpad", [(6144, 2560, 0), (200, 9728, 8), (40, 264, 0)])
+def test_fused_precomputed_mask_is_the_two_launch_path(prec, M, N, K, xpad):
+    # decode with a precomputed mask forms fl32(X + eta) inside the GEMM: bit for
+    # bit the mask kernel followed by the GEMM, and the in-stream-noise fused call
+    gp, op = PREC[prec]
+    gm, om = MECH["gaussian"]
+    sid, row0 = WL.stream_id(2, 1), 500 + M
+    X = WL.gen_x(M, K, seed=31)
+    W = WL.gen_w(N, K, seed=32)
+    Wd = dev_w(W)
+    Xd = torch.zeros((M, K + xpad), device=DEV)
+    Xd[:, :K] = dev(X)
+    Xd = Xd[:, :K]
+    eta = sp.noise(M, K, gm, 719.8, 2.0, 0, sid, row0=row0)
+    C = sp.correction(Wd, M, gm, 719.8, 2.0, 0, sid, row0, sp.SPLITEE_PREC_BF16X3)
+    Y = host(sp.masked_linear_fused(Xd, Wd, C, gm, 719.8, 2.0, 0, sid, row0, gp, eta_override=eta))
+    Y2 = host(sp.masked_linear_unmask(sp.mask(Xd, eta, gp), gp, Wd, C))
+    Y3 = host(sp.masked_linear_fused(Xd, Wd, C, gm, 719.8, 2.0, 0, sid, row0, gp))
+    assert np.array_equal(bits(Y), bits(Y2))
+    assert np.array_equal(bits(Y), bits(Y3))
+    eta_o = O.noise(M, K, om, 719.8, 2.0, 0, sid, row0)
+    b = O.error_bounds(X, eta_o, O.mask(X, eta_o), W, op)
+    assert np.all(np.abs(Y.astype(np.float64) - O.gemm64(X, W)) <= b["gate"])
 
 
 @pytest.mark.parametrize("prec", ["f32", "bf16", "bf16x3"])
