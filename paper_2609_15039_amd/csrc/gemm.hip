@@ -19,6 +19,7 @@
 // the epilogue, so results do not depend on arrival order.
 #include "common.hpp"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace {
@@ -217,14 +218,11 @@ __device__ __forceinline__ void finish_tile(const f32x4_t (&acc)[TM][TN], float*
     if (tid == 0) splitk_reset(counters + tile);
 }
 
-// --------------------------------------------------------------- bf16 MFMA
-// A K tile is 64 bf16 = 8 units of 16 bytes per row.  Tiles are fetched with
-// bounds-checked buffer loads (lanes whose row or k lies outside the matrix get
-// an offset beyond the buffer's extent and read zeros, which pads every tail)
-// into two register sets, so two K tiles are in flight while a third is
-// multiplied out of LDS.  LDS holds two stages; unit kc of row r sits at slot
-// kc ^ (r & 7), so the 16-byte fragment reads of 8 consecutive rows and the
-// stores of consecutive lanes are bank-conflict free.  One barrier per K tile.
+// ------------------------------------------------- bounds-checked buffer loads
+// Operands are read with buffer loads whose resource covers exactly the matrix:
+// a lane whose row or k lies outside it gets an offset beyond the extent and
+// reads zeros, which pads every tail.  A bfloat16 K tile is 64 k = 8 units of 16
+// bytes per row.
 
 constexpr int BK = 64;
 constexpr uint32_t OOB = 0x80000000u;
@@ -240,140 +238,7 @@ __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-template <int NPL, int BM, int BN, int WGM, int WGN>
-__global__ void __launch_bounds__(WGM * WGN * WAVE)
-gemm_bf16_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
-                 const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
-                 float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
-                 int ksplit, int kt_per_split, float* __restrict__ part, unsigned* __restrict__ counters)
-{
-    constexpr int NW = WGM * WGN;
-    constexpr int WTM = BM / WGM, WTN = BN / WGN;
-    constexpr int TM = WTM / 16, TN = WTN / 16;
-    constexpr int ROWS = NPL * BM + BN;          // LDS rows of 128 bytes per stage
-    constexpr int STAGE_BYTES = ROWS * 128;
-    constexpr int UNITS = ROWS * 8;
-    static_assert(UNITS % (NW * WAVE) == 0, "stage must split evenly over the threads");
-    constexpr int LPT = UNITS / (NW * WAVE);     // 16-byte loads per thread per stage
-    static_assert(TM * 16 == WTM && TN * 16 == WTN, "wave tile");
-
-    // two stages; the epilogue reuses the same memory for the output tile
-    constexpr int SMEM = 2 * STAGE_BYTES > (BM * (BN + 4) + 4) * 4 ? 2 * STAGE_BYTES : (BM * (BN + 4) + 4) * 4;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
-
-    const int tid = threadIdx.x, lane = tid % WAVE;
-    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
-    const int wm = wave % WGM, wn = wave / WGM;
-    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
-    const int tiles = mtiles * ntiles;
-    const int split = (int)lb / tiles, tile = (int)lb % tiles;
-    const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
-    const int ktiles = (K + BK - 1) / BK;
-    const int kt0 = split * kt_per_split;
-    const int kt1 = min(kt0 + kt_per_split, ktiles);
-    const int nk = kt1 > kt0 ? kt1 - kt0 : 0;
-
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
-
-    // unit u = tid + t * NT of the stage: row u / 8, slot u % 8, k chunk slot ^ (row & 7)
-    uint32_t goff[LPT];
-    int gkc[LPT];
-#pragma unroll
-    for (int t = 0; t < LPT; ++t) {
-        const int u = tid + t * NW * WAVE;
-        const int row = u >> 3, kc = (u & 7) ^ (row & 7);
-        gkc[t] = kc * 8;
-        if (row < NPL * BM) {
-            const int p = row / BM, r = row - p * BM, gm = m0 + r;
-            goff[t] = gm < M ? (uint32_t)((p * pstride + (int64_t)gm * lda) * 2 + kc * 16) : OOB;
-        } else {
-            const int gn = n0 + row - NPL * BM;
-            goff[t] = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + kc * 16) : OOB;
-        }
-    }
-    // Loads are issued unconditionally (tiles past this split's range read zeros)
-    // so the compiler can count the loads in flight and wait only for the oldest.
-    auto gload = [&](int kt, uint4 (&rg)[LPT]) {
-        const int kb = kt * BK;
-        const bool live = kt < kt1;
-#pragma unroll
-        for (int t = 0; t < LPT; ++t) {
-            const uint32_t off = (live && goff[t] != OOB && kb + gkc[t] < K) ? goff[t] + (uint32_t)kb * 2 : OOB;
-            // a wave's 64 units lie in 8 whole rows, all of A or all of W
-            if ((wave + t * NW) * WAVE < NPL * BM * 8) rg[t] = load16(ra, off);
-            else rg[t] = load16(rw, off);
-        }
-    };
-    auto swrite = [&](int stage, const uint4 (&rg)[LPT]) {
-        unsigned char* sb = smem + stage * STAGE_BYTES;
-#pragma unroll
-        for (int t = 0; t < LPT; ++t)
-            *reinterpret_cast<uint4*>(sb + (tid + t * NW * WAVE) * 16) = rg[t];
-    };
-
-    f32x4_t acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    uint4 r0[LPT], r1[LPT];
-    gload(kt0, r0);
-    gload(kt0 + 1, r1);
-    swrite(0, r0);
-    __syncthreads();
-
-    const int fr = lane % 16, fq = lane / 16;
-    auto compute = [&](int stage) {
-        const unsigned char* sb = smem + stage * STAGE_BYTES;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int kc = ks * 4 + fq;
-            bf16x8_t bfr[TN];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int r = NPL * BM + wn * WTN + j * 16 + fr;
-                bfr[j] = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ (r & 7)) << 4)));
-            }
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-#pragma unroll
-                for (int p = 0; p < NPL; ++p) {
-                    const int r = p * BM + wm * WTM + i * 16 + fr;
-                    const bf16x8_t af = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ (r & 7)) << 4)));
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], acc[i][j], 0, 0, 0);
-                }
-            }
-        }
-    };
-
-    // tiles go to stages 0,1,0,1,...; while stage (it % 2) is multiplied, the
-    // next tile waits in registers and the one after is being fetched
-    int it = 0;
-    // (sched_barrier keeps the prefetch ahead of the MFMAs it overlaps)
-    for (; it + 1 < nk; it += 2) {
-        gload(kt0 + it + 2, r0);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(0);
-        swrite(1, r1);
-        __syncthreads();
-        gload(kt0 + it + 3, r1);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(1);
-        swrite(0, r0);
-        __syncthreads();
-    }
-    if (it < nk) compute(0);
-
-    __syncthreads(); // every wave is done with the stage buffers
-    finish_tile<BM, BN, NW * WAVE, TM, TN, WTM, WTN, WGM>(acc, reinterpret_cast<float*>(smem), m0, n0, M, N, C, ldc,
-                                                        Out, ldo, ksplit, split, tile, part, counters);
-}
-
-// ------------------------------------------ bf16 MFMA, W streamed (M <= 128)
+// ----------------------------------------------- bf16 MFMA, W streamed (M > 16)
 // For weight-streaming shapes W is the only large operand and is read once: each
 // wave loads its own WN columns of W from HBM straight into MFMA B-operand
 // registers, D K tiles ahead of use, so W needs no LDS space, no LDS bandwidth
@@ -404,7 +269,7 @@ __device__ __forceinline__ void wait_vmem()
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-constexpr int ST_NW = 4; // waves per workgroup of the streamed kernel
+constexpr int ST_NW = 4; // waves per workgroup of the streamed kernel (WGM x WGN)
 
 // v_mfma_f32_32x32x16_bf16 operands: lane l holds row (A) or column (B) l % 32 and
 // k = 8 (l / 32) .. + 7 of a 16-wide k step; result element e of lane l is row
@@ -418,27 +283,29 @@ __device__ __forceinline__ int lds_swizzle(int r)
     return SW == 0 ? (r & 7) : ((r >> 1) & 7);
 }
 
-template <int NPL, int BM, int WN, int D, int SW = 1>
+template <int NPL, int BM, int BN, int WGM, int D, int SW = 1>
 __global__ void __launch_bounds__(ST_NW * WAVE)
 gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
                    const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
                    float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
                    int ksplit, int kt_per_split, float* __restrict__ part)
 {
-    constexpr int NW = ST_NW, BN = NW * WN;
-    constexpr int TM = BM / 32, TN = WN / 32; // 32 x 32 MFMA blocks of the wave tile
+    constexpr int NW = ST_NW, WGN = NW / WGM;
+    constexpr int WTM = BM / WGM, WTN = BN / WGN; // wave tile
+    constexpr int TM = WTM / 32, TN = WTN / 32;   // 32 x 32 MFMA blocks of the wave tile
     constexpr int S = D + 1;                  // masked-input stages = W register slots
     constexpr int AROWS = NPL * BM;           // 128-byte LDS rows per stage
     constexpr int SB = AROWS * 128;
     constexpr int LA = AROWS / 8 / NW;        // 1 KB LDS-DMA loads per wave per tile
     constexpr int LW = 4 * TN;                // W loads per wave per tile (4 k steps of 16)
-    static_assert(TM * 32 == BM && TN * 32 == WN, "wave tile");
+    static_assert(WGM * WGN == NW && TM * 32 * WGM == BM && TN * 32 * WGN == BN, "wave tile");
     static_assert(AROWS % (8 * NW) == 0, "masked-input stage must split evenly over the waves");
     static_assert(S >= 2 && S <= 4, "stages");
     static_assert((D - 1) * (LA + LW) < 64, "loads in flight exceed the wait counter");
 
     const int tid = threadIdx.x, lane = tid % WAVE;
     const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
+    const int wm = wave / WGN, wn = wave % WGN;
     const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
     const int tiles = mtiles * ntiles;
     const int split = (int)lb / tiles, tile = (int)lb % tiles;
@@ -464,12 +331,12 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
         akc[t] = kc * 8;
         aoff[t] = gm < M ? (uint32_t)((p * pstride + (int64_t)gm * lda) * 2 + kc * 16) : OOB;
     }
-    // W: lane (c = l % 32, h = l / 32) loads row n0 + WN wave + 32 j + c, 16 bytes at k = 16 s + 8 h
+    // W: lane (c = l % 32, h = l / 32) loads row n0 + WTN wn + 32 j + c, 16 bytes at k = 16 s + 8 h
     const int fc = lane % 32, fh = lane / 32;
     uint32_t woff[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-        const int gn = n0 + wave * WN + j * 32 + fc;
+        const int gn = n0 + wn * WTN + j * 32 + fc;
         woff[j] = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fh * 16) : OOB;
     }
 
@@ -515,14 +382,14 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
 
-    // fragments of k step s: every row block i and plane p
+    // fragments of k step s: every row block i of the wave tile and plane p
     auto read_a = [&](const unsigned char* sb, int s, bf16x8_t (&a)[NPL][TM]) {
         const int kc = s * 2 + fh;
 #pragma unroll
         for (int p = 0; p < NPL; ++p)
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
-                const int r = p * BM + i * 32 + fc;
+                const int r = p * BM + wm * WTM + i * 32 + fc;
                 a[p][i] = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ lds_swizzle<SW>(r)) << 4)));
             }
     };
@@ -584,11 +451,11 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int col = n0 + wave * WN + j * 32 + fc;
+                const int col = n0 + wn * WTN + j * 32 + fc;
                 if (col >= N) continue;
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int row = m0 + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
+                    const int row = m0 + wm * WTM + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
                     if (row < M) {
                         float v = acc[i][j][e];
                         if (C) v = v - C[(int64_t)row * ldc + col];
@@ -614,12 +481,12 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
 // unmask epilogue.  Thread u handles one float4 of one wave's partial (the
 // register order the partials were written in): rows 8 c + 4 (l / 32) + 0..3 of
 // block (i, j), column l % 32.
-template <int BM, int WN>
+template <int BM, int BN, int WGM>
 __global__ void __launch_bounds__(256)
 stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __restrict__ C, int64_t ldc,
                   float* __restrict__ Out, int64_t ldo, int M, int N, int mtiles, int tiles)
 {
-    constexpr int NW = ST_NW, BN = NW * WN, TM = BM / 32, TN = WN / 32;
+    constexpr int NW = ST_NW, WGN = NW / WGM, WTM = BM / WGM, WTN = BN / WGN, TM = WTM / 32, TN = WTN / 32;
     constexpr int PER_WAVE = TM * TN * 4 * 64; // float4 units
     const int64_t total = (int64_t)tiles * NW * PER_WAVE;
     const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -632,11 +499,12 @@ stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __res
     const float4* src = reinterpret_cast<const float4*>(part) + (((int64_t)tile * ksplit) * NW + wave) * PER_WAVE + e;
     f32x4_t sum = __builtin_bit_cast(f32x4_t, src[0]);
     for (int q = 1; q < ksplit; ++q) sum += __builtin_bit_cast(f32x4_t, src[(int64_t)q * NW * PER_WAVE]);
-    const int col = n0 + wave * WN + j * 32 + lane % 32;
+    const int wm = wave / WGN, wn = wave % WGN;
+    const int col = n0 + wn * WTN + j * 32 + lane % 32;
     if (col >= N) return;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int row = m0 + i * 32 + 8 * c + 4 * (lane / 32) + r;
+        const int row = m0 + wm * WTM + i * 32 + 8 * c + 4 * (lane / 32) + r;
         if (row < M) {
             float v = sum[r];
             if (C) v = v - C[(int64_t)row * ldc + col];
@@ -1037,25 +905,33 @@ struct Plan {
 
 constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 
-// The W-streamed kernel serves bfloat16 operands at 16 < M <= 128 (M <= 16 is the
-// skinny kernel's).  Variants: 10 bf16x3 BM 128, 11 bf16x3 BM 64, 12 bf16 BM 128,
-// 13 bf16 BM 64; tiles are BM x 256.  The K split fills about 256 CUs, keeps at
-// least ST_MIN_KT K tiles per split and at most ST_MAX_KS splits (measured on the
-// Llama-3.2-3B 128-token projections).
-constexpr int ST_BN = 256, ST_MIN_KT = 6, ST_MAX_KS = 12;
+// The W-streamed kernel serves every bfloat16 GEMM that does not take the skinny
+// kernel (M <= 16 with a workspace).  Tiles, measured on the Llama-3.2-3B
+// projections at 128 and 512 tokens:
+//   M <= 64:       64 x 256, 4 waves side by side  (variants 11 bf16x3, 13 bf16)
+//   64 < M <= 128: 128 x 128, 2 x 2 waves          (variants 14 bf16x3, 15 bf16)
+//   M > 128:       128 x 256, 4 waves side by side (variants 10 bf16x3, 12 bf16)
+// The K split fills about 256 CUs, keeps at least ST_MIN_KT K tiles per split and
+// at most ST_MAX_KS splits.
+constexpr int ST_MIN_KT = 6, ST_MAX_KS = 12;
 
-bool use_stream(int64_t M, int prec, int w_type)
+bool use_stream(int prec, int w_type)
 {
-    return prec != SPLITEE_PREC_F32 && w_type == SPLITEE_BF16 && M > 16 && M <= 128;
+    return prec != SPLITEE_PREC_F32 && w_type == SPLITEE_BF16;
 }
 
 Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, bool allow_split)
 {
     Plan p{};
     const bool x3 = prec == SPLITEE_PREC_BF16X3;
-    p.bm = M > 64 ? 128 : 64;
-    p.bn = ST_BN; p.bk = 64;
-    p.variant = (x3 ? 10 : 12) + (p.bm == 64 ? 1 : 0);
+    p.bk = 64;
+    if (M <= 64) {
+        p.bm = 64; p.bn = 256; p.variant = x3 ? 11 : 13;
+    } else if (M <= 128) {
+        p.bm = 128; p.bn = 128; p.variant = x3 ? 14 : 15;
+    } else {
+        p.bm = 128; p.bn = 256; p.variant = x3 ? 10 : 12;
+    }
     p.mtiles = (int)((M + p.bm - 1) / p.bm);
     p.ntiles = (int)((N + p.bn - 1) / p.bn);
     p.ktiles = (int)((K + p.bk - 1) / p.bk);
@@ -1076,17 +952,10 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, bool allow_split)
 
 Plan plan_tiled(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allow_split)
 {
-    if (use_stream(M, prec, w_type)) return plan_stream(M, N, K, prec, allow_split);
-    Plan p{};
-    if (prec == SPLITEE_PREC_F32) {
-        p.bm = 128; p.bn = 128; p.bk = 32; p.variant = 0;
-        if (M <= 64) { p.bm = 64; p.bn = 64; p.variant = 1; }
-    } else if (prec == SPLITEE_PREC_BF16X3) {
-        p.bm = 64; p.bn = 128; p.bk = 64; p.variant = 0;
-    } else {
-        p.bm = 128; p.bn = 128; p.bk = 64; p.variant = 0;
-        if (M <= 64) { p.bm = 64; p.bn = 128; p.variant = 1; }
-    }
+    if (use_stream(prec, w_type)) return plan_stream(M, N, K, prec, allow_split);
+    Plan p{}; // float32 MFMA
+    p.bm = 128; p.bn = 128; p.bk = 32; p.variant = 0;
+    if (M <= 64) { p.bm = 64; p.bn = 64; p.variant = 1; }
     (void)w_type;
     p.mtiles = (int)((M + p.bm - 1) / p.bm);
     p.ntiles = (int)((N + p.bn - 1) / p.bn);
@@ -1123,6 +992,9 @@ Plan plan_skinny(int64_t M, int64_t N, int64_t K, int prec)
     p.ntiles = (int)((N + SK_BN - 1) / SK_BN);
     p.ktiles = (int)((K + 31) / 32);
     int ks = SK_TARGET_WGS / p.ntiles; // whole rounds only: a partial second round costs a full one
+    // more than 256 tiles: split up to 1024 workgroups while every split still fills
+    // the W ring (measured on the Qwen3-4B gate/up projection, 304 tiles)
+    if (p.ntiles > 256) ks = std::max(1, std::min(p.ktiles / SK_RING, 1024 / p.ntiles));
     if (ks > p.ktiles) ks = p.ktiles;
     if (ks < 1) ks = 1;
     int sps = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
@@ -1181,32 +1053,27 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         const int64_t planes = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
         if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
             return SPLITEE_ERR_UNSUPPORTED;
-        if (p.variant >= 10) {
-            float* pp = reinterpret_cast<float*>(ws);
-#define ST_LAUNCH(NP, BM_, D_) hipLaunchKernelGGL((gemm_stream_kernel<NP, BM_, 64, D_>), grid, dim3(ST_NW * WAVE), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
-            switch (p.variant) {
-            case 10: ST_LAUNCH(3, 128, 2); break;
-            case 11: ST_LAUNCH(3, 64, 3); break;
-            case 12: ST_LAUNCH(1, 128, 2); break;
-            default: ST_LAUNCH(1, 64, 3); break;
-            }
+        float* pp = reinterpret_cast<float*>(ws);
+#define ST_LAUNCH(NP, BM_, BN_, WGM_, D_) hipLaunchKernelGGL((gemm_stream_kernel<NP, BM_, BN_, WGM_, D_>), grid, dim3(ST_NW * WAVE), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
+        switch (p.variant) {
+        case 10: ST_LAUNCH(3, 128, 256, 1, 2); break;
+        case 11: ST_LAUNCH(3, 64, 256, 1, 3); break;
+        case 12: ST_LAUNCH(1, 128, 256, 1, 2); break;
+        case 13: ST_LAUNCH(1, 64, 256, 1, 3); break;
+        case 14: ST_LAUNCH(3, 128, 128, 2, 2); break;
+        default: ST_LAUNCH(1, 128, 128, 2, 2); break;
+        }
 #undef ST_LAUNCH
-            if (p.ksplit > 1) {
-                const int tiles = p.mtiles * p.ntiles;
-                const int64_t units = (int64_t)tiles * ST_NW * (p.bm / 32) * 2 * 4 * WAVE;
-                const dim3 g2((unsigned)((units + 255) / 256));
-                if (p.bm == 128)
-                    hipLaunchKernelGGL((stream_sum_kernel<128, 64>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
-                else
-                    hipLaunchKernelGGL((stream_sum_kernel<64, 64>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
-            }
-        } else if (prec == SPLITEE_PREC_BF16) {
-            if (p.variant == 0)
-                hipLaunchKernelGGL((gemm_bf16_kernel<1, 128, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+        if (p.ksplit > 1) {
+            const int tiles = p.mtiles * p.ntiles;
+            const int64_t units = (int64_t)tiles * p.bm * p.bn / 4; // float4 units of the partial tiles
+            const dim3 g2((unsigned)((units + 255) / 256));
+            if (p.variant >= 14)
+                hipLaunchKernelGGL((stream_sum_kernel<128, 128, 2>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
+            else if (p.bm == 128)
+                hipLaunchKernelGGL((stream_sum_kernel<128, 256, 1>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
             else
-                hipLaunchKernelGGL((gemm_bf16_kernel<1, 64, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
-        } else {
-            hipLaunchKernelGGL((gemm_bf16_kernel<3, 64, 128, 2, 2>), grid, dim3(256), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
+                hipLaunchKernelGGL((stream_sum_kernel<64, 256, 1>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
         }
     }
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
