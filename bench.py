@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (HBM counter calibration) and exit")
+    ap.add_argument("--counter-launches", type=int, default=0,
+                    help="only run each projection group's GEMM launch this many times, eagerly and in order "
+                         "(for rocprofv3 counter runs), and exit")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample")
     return ap.parse_args()
@@ -116,8 +119,10 @@ class Path:
         self.decode = M <= 16 and prec != sp.SPLITEE_PREC_F32
         for p in self.projs:
             self.ws.append(sp.workspace(M, p.N, p.K, prec, dev, gemm_only=not self.decode))
-        self.eta = [torch.empty((M, p.K), dtype=torch.float32, device=dev) for p in self.projs] \
-            if self.decode else None
+        # decode: the masks of every layer of a step, [layer][token][k] per projection group
+        self.eta = [torch.empty((self.layers_per_step, M, p.K), dtype=torch.float32, device=dev)
+                    for p in self.projs] if self.decode else None
+        self.sid_step = WL.stream_id(1, 0) - WL.stream_id(0, 0)
         self.W, self.C, self.sid = [], [], []
         for l in range(nlayers):
             Ws, sids = [], []
@@ -153,22 +158,28 @@ class Path:
         if self.decode:
             self.sp.splitee_masked_linear_fused(
                 self.X[i], p.K, W, self.wt, p.K, C, C.stride(0), self.Y[i], p.N, M, p.N, p.K, self.mech,
-                self.delta, self.eps, 0, self.sid[l][i], self.row0, self.eta[i], self.prec,
+                self.delta, self.eps, 0, self.sid[l][i], self.row0, self.eta[i][l % self.layers_per_step], self.prec,
                 self.ws[i][0], self.ws[i][1])
         else:
             self.sp.splitee_masked_linear_unmask(self.Xt[i], self.prec, p.K, W, self.wt, p.K, C,
                                                  C.stride(0), self.Y[i], p.N, M, p.N, p.K,
                                                  self.ws[i][0], self.ws[i][1])
 
+    def draw_masks(self, base):
+        """Decode: one launch draws the masks of all layers and projection groups of a step."""
+        Ks = [p.K for p in self.projs]
+        self.sp.splitee_noise_gen_multi(self.eta, Ks, Ks, self.sid[base], self.M, self.mech, self.delta,
+                                        self.eps, 0, self.row0, reps=self.layers_per_step,
+                                        rep_strides=[self.M * K for K in Ks], rep_sid_step=self.sid_step)
+
     def launches(self, s):
         """All kernels of step s: noise, mask, GEMM and unmask of every projection."""
         sp, M = self.sp, self.M
         base = (s % self.nsets) * self.layers_per_step
+        if self.decode:
+            self.draw_masks(base)
         for l in range(base, base + self.layers_per_step):
             if self.decode:
-                Ks = [p.K for p in self.projs]
-                sp.splitee_noise_gen_multi(self.eta, Ks, Ks, self.sid[l], M, self.mech, self.delta,
-                                           self.eps, 0, self.row0)
                 for i in range(len(self.projs)):
                     self.gemm(l, i)
                 continue
@@ -331,6 +342,26 @@ def measured_traffic(workload, prec_name, names):
     return rows
 
 
+def counter_launches(torch, sp, WL, args, prec):
+    """The GEMM launches alone, for counter collection: after set-up, `n` rounds of
+    one launch per projection group (layer 0), in projection order, each followed by
+    a device synchronization; these are the run's last dispatches."""
+    path = Path(torch, sp, WL, args.workload, prec, sp.MECHS[args.mech], args.delta, args.eps, 1)
+    if path.decode:
+        path.draw_masks(0)
+    else:
+        for i, p in enumerate(path.projs):
+            sp.splitee_noise_mask(path.X[i], p.K, path.Xt[i], path.prec, p.K, path.M, p.K, path.mech,
+                                  path.delta, path.eps, 0, path.sid[0][i], path.row0)
+    torch.cuda.synchronize()
+    for _ in range(args.counter_launches):
+        for i in range(len(path.projs)):
+            path.gemm(0, i)
+            torch.cuda.synchronize()
+    print(json.dumps({"counter_launches": args.counter_launches, "projections": [p.name for p in path.projs],
+                      "algorithmic_bytes": [int(b) for b in path.gemm_bytes()]}), flush=True)
+
+
 def copy_probe(mib):
     import torch
     n = mib * (1 << 20) // 4
@@ -363,6 +394,9 @@ def main():
     prec = sp.PRECS[args.prec]
     if args.workload == "single-fp32-m32":
         prec = sp.SPLITEE_PREC_F32
+    if args.counter_launches:
+        counter_launches(torch, sp, WL, args, prec)
+        return
     path, ms, per_proj_us = run_mode(torch, sp, WL, args.workload, prec, args, args.steps, args.warmup)
     flops = path.flops()
     value = flops / (ms * 1e-3) / 1e12

@@ -112,21 +112,28 @@ int splitee_noise_gen(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech
                       uint64_t row0, void* stream);
 
 /*
- * Several noise blocks in one launch: block q is what splitee_noise_gen(eta[q],
- * ld_eta[q], M, K[q], mech, sensitivity, epsilon, seed, stream_id[q], row0, stream)
- * writes, element for element.  The blocks share M, the mechanism, seed and row0;
- * each has its own K, leading dimension and stream id.  This is the per-layer
- * precomputation of the masks (Sec. "Precomputing the Mask and Noise
- * Correction"): one launch fills the masks of all projections of a layer.
- *   eta, ld_eta, K, stream_id   host arrays of `count` entries (1 <= count <= 8,
- *                               count == 0 does nothing); eta[q] a device pointer,
- *                               16-byte aligned, ld_eta[q] >= K[q], a multiple of 4
- * Requires K[q] % 4 == 0.  The host arrays are read during the call only.
+ * Several noise blocks in one launch: block (q, r), q < count, r < reps, is what
+ * splitee_noise_gen(eta[q] + r * rep_stride[q], ld_eta[q], M, K[q], mech, sensitivity,
+ * epsilon, seed, stream_id[q] + r * rep_sid_step, row0, stream) writes, element for
+ * element.  The blocks share M, the mechanism, seed and row0; each q has its own K,
+ * leading dimension, stream id and repetition stride, and repetition r steps
+ * block q's output by rep_stride[q] elements and its stream id by rep_sid_step.  This is the
+ * precomputation of the masks (Sec. "Precomputing the Mask and Noise Correction"):
+ * one launch draws the masks of all projections of a layer, or of all layers
+ * (r = layer) for one decode step.
+ *   eta, ld_eta, K, stream_id   host arrays of `count` entries (0 <= count <= 8);
+ *                               eta[q] a device pointer, 16-byte aligned, ld_eta[q]
+ *                               >= K[q], a multiple of 4
+ *   reps                        0 <= reps <= 65535 (count or reps 0: nothing to do)
+ *   rep_stride                  host array of `count` strides in elements, >= 0 and a
+ *                               multiple of 4 (may be NULL when reps <= 1)
+ * Requires K[q] % 4 == 0.  The host arrays are read during the call only.  Blocks
+ * must not overlap in memory.
  */
 int splitee_noise_gen_multi(float* const* eta, const int64_t* ld_eta, const int64_t* K,
-                            const uint64_t* stream_id, int count, int64_t M, int mech,
-                            double sensitivity, double epsilon, uint64_t seed, uint64_t row0,
-                            void* stream);
+                            const uint64_t* stream_id, int count, int reps, const int64_t* rep_stride,
+                            uint64_t rep_sid_step, int64_t M, int mech, double sensitivity,
+                            double epsilon, uint64_t seed, uint64_t row0, void* stream);
 
 /*
  * Mask: Xt = fl32(X + eta) (the vector addition of Sec. "Offloading Linear

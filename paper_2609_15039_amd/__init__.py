@@ -66,7 +66,7 @@ def load():
         "splitee_gemm_workspace_bytes": (SZ, [I64, I64, I64, I]),
         "splitee_masked_linear_unmask": (I, [P, I, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, P,
                                              SZ, P]),
-        "splitee_noise_gen_multi": (I, [P, P, P, P, I, I64, I, D, D, U64, U64, P]),
+        "splitee_noise_gen_multi": (I, [P, P, P, P, I, I, P, U64, I64, I, D, D, U64, U64, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -127,8 +127,9 @@ def splitee_noise_gen(eta, ld_eta, M, K, mech, sensitivity, epsilon, seed, strea
 
 
 def splitee_noise_gen_multi(etas, ld_etas, Ks, stream_ids, M, mech, sensitivity, epsilon, seed,
-                            row0=0, stream=None):
-    """etas, ld_etas, Ks, stream_ids: sequences of equal length (the noise blocks)."""
+                            row0=0, reps=1, rep_strides=None, rep_sid_step=0, stream=None):
+    """etas, ld_etas, Ks, stream_ids (and rep_strides when reps > 1): sequences of
+    equal length, one entry per noise block."""
     n = len(etas)
     if not (len(ld_etas) == len(Ks) == len(stream_ids) == n):
         raise ValueError("splitee_noise_gen_multi: per-block sequences differ in length")
@@ -136,9 +137,15 @@ def splitee_noise_gen_multi(etas, ld_etas, Ks, stream_ids, M, mech, sensitivity,
     lds = (ctypes.c_int64 * max(n, 1))(*ld_etas)
     ks = (ctypes.c_int64 * max(n, 1))(*Ks)
     sids = (ctypes.c_uint64 * max(n, 1))(*stream_ids)
+    strides = None
+    if rep_strides is not None:
+        if len(rep_strides) != n:
+            raise ValueError("splitee_noise_gen_multi: rep_strides differs in length")
+        strides = ctypes.cast((ctypes.c_int64 * max(n, 1))(*rep_strides), ctypes.c_void_p)
     _check("splitee_noise_gen_multi", load().splitee_noise_gen_multi(
         ctypes.cast(ptrs, ctypes.c_void_p), ctypes.cast(lds, ctypes.c_void_p), ctypes.cast(ks, ctypes.c_void_p),
-        ctypes.cast(sids, ctypes.c_void_p), n, M, mech, sensitivity, epsilon, seed, row0, _stream(stream)))
+        ctypes.cast(sids, ctypes.c_void_p), n, reps, strides, rep_sid_step, M, mech, sensitivity, epsilon,
+        seed, row0, _stream(stream)))
 
 
 def splitee_mask(X, ldx, eta, ld_eta, Xt, out_prec, ldxt, M, K, stream=None):

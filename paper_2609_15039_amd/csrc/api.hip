@@ -144,23 +144,27 @@ int splitee_noise_gen(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech
 }
 
 int splitee_noise_gen_multi(float* const* eta, const int64_t* ld_eta, const int64_t* K,
-                            const uint64_t* stream_id, int count, int64_t M, int mech, double sensitivity,
-                            double epsilon, uint64_t seed, uint64_t row0, void* stream)
+                            const uint64_t* stream_id, int count, int reps, const int64_t* rep_stride,
+                            uint64_t rep_sid_step, int64_t M, int mech, double sensitivity, double epsilon,
+                            uint64_t seed, uint64_t row0, void* stream)
 {
     int rc = check_noise_args(mech, sensitivity, epsilon);
     if (rc) return rc;
-    if (count < 0 || count > splitee::NOISE_MULTI_MAX) return SPLITEE_ERR_ARG;
-    if (count == 0) return SPLITEE_OK;
+    if (count < 0 || count > splitee::NOISE_MULTI_MAX || reps < 0 || reps > 65535) return SPLITEE_ERR_ARG;
+    if (count == 0 || reps == 0) return SPLITEE_OK;
     if (!eta || !ld_eta || !K || !stream_id) return SPLITEE_ERR_ARG;
+    if (reps > 1 && !rep_stride) return SPLITEE_ERR_ARG;
     if (!dims_ok(M, 0, 0)) return SPLITEE_ERR_SHAPE;
     for (int q = 0; q < count; ++q) {
         if (!dims_ok(M, 0, K[q]) || K[q] % 4 != 0 || ld_eta[q] < K[q]) return SPLITEE_ERR_SHAPE;
+        if (reps > 1 && rep_stride[q] < 0) return SPLITEE_ERR_SHAPE;
+        if (reps > 1 && rep_stride[q] % 4 != 0) return SPLITEE_ERR_ALIGN;
         if (M > 0 && K[q] > 0 && !eta[q]) return SPLITEE_ERR_ARG;
         if (eta[q] && (!aligned16(eta[q]) || !pitch16(ld_eta[q], 4))) return SPLITEE_ERR_ALIGN;
     }
     if (M == 0) return SPLITEE_OK;
-    return splitee_host::launch_noise_multi(eta, ld_eta, K, stream_id, count, M, mech, sensitivity / epsilon,
-                                            seed, row0, as_stream(stream));
+    return splitee_host::launch_noise_multi(eta, ld_eta, K, stream_id, count, reps, rep_stride, rep_sid_step, M,
+                                            mech, sensitivity / epsilon, seed, row0, as_stream(stream));
 }
 
 int splitee_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, void* Xt,

@@ -53,7 +53,8 @@ namespace splitee_host {
 int launch_noise(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech, double scale,
                  uint64_t seed, uint64_t sid, uint64_t row0, hipStream_t s);
 int launch_noise_multi(float* const* eta, const int64_t* ld, const int64_t* K, const uint64_t* sid, int count,
-                       int64_t M, int mech, double scale, uint64_t seed, uint64_t row0, hipStream_t s);
+                       int reps, const int64_t* rep_stride, uint64_t rep_sid_step, int64_t M, int mech,
+                       double scale, uint64_t seed, uint64_t row0, hipStream_t s);
 int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int gen_mech,
                 double scale, uint64_t seed, uint64_t sid, uint64_t row0, void* Xt, int prec,
                 int64_t ldxt, int64_t plane_stride, int64_t M, int64_t K,

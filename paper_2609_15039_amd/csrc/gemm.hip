@@ -481,12 +481,12 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
 // unmask epilogue.  Thread u handles one float4 of one wave's partial (the
 // register order the partials were written in): rows 8 c + 4 (l / 32) + 0..3 of
 // block (i, j), column l % 32.
-template <int BM, int BN, int WGM>
+template <int BM, int BN, int WGM, int WGN = ST_NW / WGM>
 __global__ void __launch_bounds__(256)
 stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __restrict__ C, int64_t ldc,
                   float* __restrict__ Out, int64_t ldo, int M, int N, int mtiles, int tiles)
 {
-    constexpr int NW = ST_NW, WGN = NW / WGM, WTM = BM / WGM, WTN = BN / WGN, TM = WTM / 32, TN = WTN / 32;
+    constexpr int NW = WGM * WGN, WTM = BM / WGM, WTN = BN / WGN, TM = WTM / 32, TN = WTN / 32;
     constexpr int PER_WAVE = TM * TN * 4 * 64; // float4 units
     const int64_t total = (int64_t)tiles * NW * PER_WAVE;
     const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

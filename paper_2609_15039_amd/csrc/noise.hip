@@ -28,21 +28,26 @@ __global__ void __launch_bounds__(256) noise_kernel(float* __restrict__ eta, int
 }
 
 // Several noise blocks (same M, row0, mechanism and scale; own K, stream_id and
-// output) in one launch: thread t handles pair t of the concatenation of the
-// blocks' M x K / 2 pairs.
+// output) in one launch, each repeated `reps` times: repetition r of block q
+// writes at eta[q] + r * rep_stride[q] with stream id sid[q] + r * rep_sid_step.
+// blockIdx.y is the repetition; thread t of it handles pair t of the
+// concatenation of the blocks' M x K / 2 pairs.
 struct NoiseBlocks {
     float* eta[splitee::NOISE_MULTI_MAX];
     int64_t ld[splitee::NOISE_MULTI_MAX];
     int64_t K[splitee::NOISE_MULTI_MAX];
     uint64_t sid[splitee::NOISE_MULTI_MAX];
     int64_t first[splitee::NOISE_MULTI_MAX + 1]; // prefix sums of the blocks' pair counts
+    int64_t rep_stride[splitee::NOISE_MULTI_MAX];
     int count;
+    uint64_t rep_sid_step;
 };
 
-__global__ void __launch_bounds__(256) noise_multi_kernel(NoiseBlocks nb, int64_t M, int mech, double scale,
-                                                          uint64_t seed, uint64_t row0)
+__global__ void __launch_bounds__(256) noise_multi_kernel(NoiseBlocks nb, int mech, double scale, uint64_t seed,
+                                                          uint64_t row0)
 {
     const int64_t total = nb.first[nb.count];
+    const int64_t r = blockIdx.y;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
          t += (int64_t)gridDim.x * blockDim.x) {
@@ -51,11 +56,10 @@ __global__ void __launch_bounds__(256) noise_multi_kernel(NoiseBlocks nb, int64_
         const int64_t K = nb.K[q], ppr = K >> 1, u = t - nb.first[q];
         const int64_t i = u / ppr, c = u - i * ppr;
         const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)(K >> 2) + (uint64_t)(c >> 1);
-        const uint64_t sid = nb.sid[q];
+        const uint64_t sid = nb.sid[q] + (uint64_t)r * nb.rep_sid_step;
         const float2 v = noise_pair(mech, scale, b, (int)(c & 1), (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
-        *reinterpret_cast<float2*>(nb.eta[q] + i * nb.ld[q] + 2 * c) = v;
+        *reinterpret_cast<float2*>(nb.eta[q] + r * nb.rep_stride[q] + i * nb.ld[q] + 2 * c) = v;
     }
-    (void)M;
 }
 
 // Xt = fl32(X + eta) for 2 elements per thread; eta is generated (gen = true) or
@@ -192,7 +196,8 @@ int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, i
 }
 
 int launch_noise_multi(float* const* eta, const int64_t* ld, const int64_t* K, const uint64_t* sid, int count,
-                       int64_t M, int mech, double scale, uint64_t seed, uint64_t row0, hipStream_t s)
+                       int reps, const int64_t* rep_stride, uint64_t rep_sid_step, int64_t M, int mech,
+                       double scale, uint64_t seed, uint64_t row0, hipStream_t s)
 {
     NoiseBlocks nb{};
     nb.count = count;
@@ -202,12 +207,14 @@ int launch_noise_multi(float* const* eta, const int64_t* ld, const int64_t* K, c
         nb.ld[q] = ld[q];
         nb.K[q] = K[q];
         nb.sid[q] = sid[q];
+        nb.rep_stride[q] = rep_stride ? rep_stride[q] : 0;
         nb.first[q + 1] = nb.first[q] + M * (K[q] / 2);
     }
+    nb.rep_sid_step = rep_sid_step;
     const int64_t work = nb.first[count];
-    if (work == 0) return SPLITEE_OK;
-    hipLaunchKernelGGL(noise_multi_kernel, dim3(grid_for(work, 256)), dim3(256), 0, s, nb, M, mech, scale, seed,
-                       row0);
+    if (work == 0 || reps == 0) return SPLITEE_OK;
+    hipLaunchKernelGGL(noise_multi_kernel, dim3(grid_for(work, 256), (unsigned)reps), dim3(256), 0, s, nb, mech,
+                       scale, seed, row0);
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 

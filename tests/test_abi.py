@@ -61,22 +61,27 @@ def test_noise_gen_validation(lib, kw, code):
     assert noise(lib, **kw) == code
 
 
-def noise_multi(lib, etas=(P, P), lds=(8, 16), ks=(8, 16), sids=(0, 1), count=None, M=2, mech=G,
-                d=1.0, e=1.0, null_arrays=False):
+def noise_multi(lib, etas=(P, P), lds=(8, 16), ks=(8, 16), sids=(0, 1), count=None, reps=2,
+                rep_strides=(64, 64), rep_sid_step=256, M=2, mech=G, d=1.0, e=1.0, null_arrays=False):
     n = len(etas)
     arr = lambda t, v: (t * max(n, 1))(*v)
     a = [arr(ctypes.c_void_p, etas), arr(ctypes.c_int64, lds), arr(ctypes.c_int64, ks),
          arr(ctypes.c_uint64, sids)]
     a = [None if null_arrays else ctypes.cast(x, ctypes.c_void_p) for x in a]
-    return lib.splitee_noise_gen_multi(*a, n if count is None else count, M, mech, d, e, 0, 0, None)
+    st = None if rep_strides is None else ctypes.cast(arr(ctypes.c_int64, rep_strides), ctypes.c_void_p)
+    return lib.splitee_noise_gen_multi(*a, n if count is None else count, reps, st, rep_sid_step, M,
+                                       mech, d, e, 0, 0, None)
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(e=0.0), ARG), (dict(d=math.inf), ARG), (dict(mech=5), ARG),
     (dict(count=9), ARG), (dict(count=-1), ARG), (dict(null_arrays=True), ARG),
+    (dict(reps=-1), ARG), (dict(reps=65536), ARG), (dict(rep_strides=None), ARG),
+    (dict(rep_strides=(64, -4)), SHAPE), (dict(rep_strides=(6, 64)), ALIGN),
     (dict(ks=(8, 6)), SHAPE), (dict(lds=(8, 12)), SHAPE), (dict(M=-3), SHAPE),
     (dict(etas=(P, 8)), ALIGN), (dict(lds=(8, 18)), ALIGN), (dict(etas=(P, None)), ARG),
-    (dict(count=0, null_arrays=True), OK), (dict(M=0), OK),
+    (dict(count=0, null_arrays=True), OK), (dict(reps=0, null_arrays=True), OK), (dict(M=0), OK),
+    (dict(reps=1, rep_strides=None, M=0), OK),
     (dict(etas=(None, None), ks=(0, 0), lds=(0, 0)), OK)])
 def test_noise_gen_multi_validation(lib, kw, code):
     assert noise_multi(lib, **kw) == code

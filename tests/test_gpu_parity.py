@@ -127,6 +127,25 @@ def test_noise_gen_multi_eight_blocks_equal_single_calls():
         assert torch.equal(eta.view(torch.int32), one.view(torch.int32))
 
 
+@pytest.mark.parametrize("mech", ["laplace", "gaussian"])
+def test_noise_gen_multi_repetitions_are_layers(mech):
+    # repetition r of block q: output at eta[q] + r * rep_strides[q], stream id sid[q] + 256 r,
+    # i.e. the masks of layer r when stream ids are (layer << 8) | group
+    g, o = MECH[mech]
+    M, L, row0, seed = 3, 5, 1024, 11
+    Ks = (2560, 4096, 9728)
+    bufs = [torch.full((L, M, K + 4), float("nan"), device=DEV) for K in Ks]
+    sids = [WL.stream_id(0, q) for q in range(len(Ks))]
+    sp.splitee_noise_gen_multi(bufs, [K + 4 for K in Ks], Ks, sids, M, g, 719.8, 2.0, seed, row0, reps=L,
+                               rep_strides=[M * (K + 4) for K in Ks], rep_sid_step=256)
+    for q, (buf, K) in enumerate(zip(bufs, Ks)):
+        got = host(buf)
+        for r in range(L):
+            ref = O.noise(M, K, o, 719.8, 2.0, seed, WL.stream_id(r, q), row0)
+            assert np.array_equal(bits(got[r, :, :K]), bits(ref)), (q, r)
+        assert np.all(np.isnan(got[:, :, K:]))
+
+
 # ------------------------------------------------------------------------- mask
 
 @pytest.mark.parametrize("prec", ["f32", "bf16", "bf16x3"])
