@@ -270,6 +270,7 @@ __device__ __forceinline__ void wait_vmem()
 }
 
 constexpr int ST_NW = 4; // waves per workgroup of the streamed kernel (WGM x WGN)
+constexpr int ST_MIN_KT = 6, ST_MAX_KS = 12; // K split of the streamed kernel
 
 // v_mfma_f32_32x32x16_bf16 operands: lane l holds row (A) or column (B) l % 32 and
 // k = 8 (l / 32) .. + 7 of a 16-wide k step; result element e of lane l is row
@@ -497,18 +498,32 @@ stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __res
     const int lane = e % 64, ijc = e / 64, c = ijc % 4, ij = ijc / 4, i = ij / TN, j = ij % TN;
     const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
     const float4* src = reinterpret_cast<const float4*>(part) + (((int64_t)tile * ksplit) * NW + wave) * PER_WAVE + e;
-    f32x4_t sum = __builtin_bit_cast(f32x4_t, src[0]);
-    for (int q = 1; q < ksplit; ++q) sum += __builtin_bit_cast(f32x4_t, src[(int64_t)q * NW * PER_WAVE]);
     const int wm = wave / WGN, wn = wave % WGN;
     const int col = n0 + wn * WTN + j * 32 + lane % 32;
+    const int row0 = m0 + wm * WTM + i * 32 + 8 * c + 4 * (lane / 32);
+    // C first, then every split's partial: all loads in flight together
+    float cv[4] = {0.f, 0.f, 0.f, 0.f};
+    if (C && col < N) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            if (row0 + r < M) cv[r] = C[(int64_t)(row0 + r) * ldc + col];
+    }
+    f32x4_t v[ST_MAX_KS];
+#pragma unroll
+    for (int q = 0; q < ST_MAX_KS; ++q)
+        v[q] = q < ksplit ? __builtin_bit_cast(f32x4_t, src[(int64_t)q * NW * PER_WAVE]) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    f32x4_t sum = v[0];
+#pragma unroll
+    for (int q = 1; q < ST_MAX_KS; ++q)
+        if (q < ksplit) sum += v[q];
     if (col >= N) return;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * WTM + i * 32 + 8 * c + 4 * (lane / 32) + r;
+        const int row = row0 + r;
         if (row < M) {
-            float v = sum[r];
-            if (C) v = v - C[(int64_t)row * ldc + col];
-            Out[(int64_t)row * ldo + col] = v;
+            float y = sum[r];
+            if (C) y = y - cv[r];
+            Out[(int64_t)row * ldo + col] = y;
         }
     }
 }
@@ -913,7 +928,6 @@ constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 //   M > 128:       128 x 256, 4 waves side by side (variants 10 bf16x3, 12 bf16)
 // The K split fills about 256 CUs, keeps at least ST_MIN_KT K tiles per split and
 // at most ST_MAX_KS splits.
-constexpr int ST_MIN_KT = 6, ST_MAX_KS = 12;
 
 bool use_stream(int prec, int w_type)
 {
