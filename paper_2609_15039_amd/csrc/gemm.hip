@@ -908,6 +908,193 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
     if (tid == 0) splitk_reset(counters + tile);
 }
 
+// ---------------------------------------------------------------- GEMV (M <= 2)
+// Decode with one or two tokens is a matrix-vector product bound by the single
+// pass over W, so it runs on the vector ALUs: a wave owns `ppw` consecutive pairs
+// of W rows (output columns) and the whole of K, so no K split and no hand-off
+// between workgroups is needed; the grid is at most two workgroups per CU and
+// the W ring runs on across a wave's row pairs.  The workgroup first writes the masked
+// input x~ (M x K float32) to LDS: fl32(X + eta), or the sum of its bfloat16
+// planes (exact: the planes split a float32 exactly), rounded to bfloat16 for the
+// single-plane precision.  The W loads of the first GV_RING chunks are issued
+// before the masked-input loads, so that the two latencies overlap (loads
+// complete in order).  Lane l then streams k = 512 j + 8 l .. + 7 of its rows
+// (16-byte loads, GV_RING chunks in flight), accumulates fma(x~, w, acc) in
+// float32 in k order, and the wave sums its lanes with a fixed butterfly.
+
+constexpr int GV_WAVES = 4;  // waves per workgroup
+constexpr int GV_NR = 2;     // W rows per wave
+constexpr int GV_RING = 8;   // 512-k chunks per row in flight
+constexpr int GV_XR = 2;     // masked-input units (8 k) per thread per load round
+constexpr int GV_MMAX = 2;   // largest M
+constexpr int GV_MAX_WGS = 1024; // four workgroups per CU
+
+__device__ __forceinline__ float gv_wave_sum(float v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
+    return v;
+}
+
+template <int NPL, bool MASK, int MR>
+__global__ void __launch_bounds__(GV_WAVES * WAVE)
+gemv_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
+            float* __restrict__ Out, int64_t ldo, int N, int K, int ppw)
+{
+    extern __shared__ __attribute__((aligned(16))) float xs[]; // MR x K
+    constexpr int NT = GV_WAVES * WAVE;
+    const int tid = threadIdx.x, lane = tid % WAVE;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int n0 = ((int)lb * GV_WAVES + wave) * GV_NR * ppw; // first row of the wave
+
+    // 1. the W ring, then x~ to LDS (8 consecutive k per unit, GV_XR units per thread and round)
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
+    const int nchunk = (K + 511) / 512;
+    const int units_w = ppw * nchunk; // (row pair, 512-k chunk) units of the wave, pair-major
+    auto wload = [&](int r, int t) {
+        const int pr = t / nchunk, j = t - pr * nchunk;
+        const int n = n0 + pr * GV_NR + r, k = 512 * j + 8 * lane;
+        const bool ok = t < units_w && n < N && k < K;
+        return load16(rw, ok ? (uint32_t)(((int64_t)n * ldw + k) * 2) : OOB);
+    };
+    uint4 ring[GV_RING][GV_NR];
+#pragma unroll
+    for (int t = 0; t < GV_RING; ++t)
+#pragma unroll
+        for (int r = 0; r < GV_NR; ++r) ring[t][r] = wload(r, t);
+
+    const int upr = K / 8, units = MR * upr;
+    for (int u0 = 0; u0 < units; u0 += GV_XR * NT) {
+        float x[GV_XR][8];
+        if (MASK) {
+            float4 xv[GV_XR][2], ev[GV_XR][2];
+#pragma unroll
+            for (int i = 0; i < GV_XR; ++i) {
+                const int u = u0 + i * NT + tid;
+                const int m = u < units ? u / upr : 0, k = u < units ? (u - m * upr) * 8 : 0;
+                const float4* xp = reinterpret_cast<const float4*>(src.X + (int64_t)m * src.ldx + k);
+                const float4* ep = reinterpret_cast<const float4*>(src.eta + (int64_t)m * src.ld_eta + k);
+                xv[i][0] = xp[0]; xv[i][1] = xp[1]; ev[i][0] = ep[0]; ev[i][1] = ep[1];
+            }
+#pragma unroll
+            for (int i = 0; i < GV_XR; ++i) {
+                const float* a = reinterpret_cast<const float*>(xv[i]);
+                const float* e = reinterpret_cast<const float*>(ev[i]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float v = a[q] + e[q];
+                    if (NPL == 1) v = splitee::bf16_bits_to_f32(splitee::bf16_bits_rne(v));
+                    x[i][q] = v;
+                }
+            }
+        } else {
+            uint4 pl[GV_XR][NPL];
+#pragma unroll
+            for (int i = 0; i < GV_XR; ++i) {
+                const int u = u0 + i * NT + tid;
+                const int m = u < units ? u / upr : 0, k = u < units ? (u - m * upr) * 8 : 0;
+#pragma unroll
+                for (int p = 0; p < NPL; ++p)
+                    pl[i][p] = *reinterpret_cast<const uint4*>(src.A + p * src.pstride + (int64_t)m * src.lda + k);
+            }
+#pragma unroll
+            for (int i = 0; i < GV_XR; ++i)
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float v = 0.f;
+#pragma unroll
+                    for (int p = 0; p < NPL; ++p) {
+                        const uint32_t wd = reinterpret_cast<const uint32_t*>(&pl[i][p])[q / 2];
+                        const float t = splitee::bf16_bits_to_f32((q & 1) ? (wd >> 16) : (wd & 0xFFFFu));
+                        v = p == 0 ? t : v + t; // hi + mid, then + lo: exact
+                    }
+                    x[i][q] = v;
+                }
+        }
+#pragma unroll
+        for (int i = 0; i < GV_XR; ++i) {
+            const int u = u0 + i * NT + tid;
+            if (u < units) {
+                const int m = u / upr, k = (u - m * upr) * 8;
+                *reinterpret_cast<float4*>(xs + (int64_t)m * K + k) = make_float4(x[i][0], x[i][1], x[i][2], x[i][3]);
+                *reinterpret_cast<float4*>(xs + (int64_t)m * K + k + 4) = make_float4(x[i][4], x[i][5], x[i][6], x[i][7]);
+            }
+        }
+    }
+    __syncthreads();
+
+    // 2. stream the wave's rows (waves past N run on zeros and store nothing)
+    float acc[MR][GV_NR];
+#pragma unroll
+    for (int m = 0; m < MR; ++m)
+#pragma unroll
+        for (int r = 0; r < GV_NR; ++r) acc[m][r] = 0.f;
+    // unit t = (row pair pr, chunk j); the ring refill is unit t + GV_RING = (prr, jr).
+    // The masked input of the next unit is read from LDS while this one is multiplied.
+    auto load_x = [&](float (&x)[MR][8], int j) {
+        const int k = 512 * j + 8 * lane;
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+            float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+            if (k < K) {
+                a = *reinterpret_cast<const float4*>(xs + (int64_t)m * K + k);
+                b = *reinterpret_cast<const float4*>(xs + (int64_t)m * K + k + 4);
+            }
+            x[m][0] = a.x; x[m][1] = a.y; x[m][2] = a.z; x[m][3] = a.w;
+            x[m][4] = b.x; x[m][5] = b.y; x[m][6] = b.z; x[m][7] = b.w;
+        }
+    };
+    const int nloop = (units_w + GV_RING - 1) / GV_RING * GV_RING;
+    int pr = 0, j = 0;
+    int prr = GV_RING / nchunk, jr = GV_RING - (GV_RING / nchunk) * nchunk;
+    float xc[MR][8];
+    load_x(xc, 0);
+    for (int t0 = 0; t0 < nloop; t0 += GV_RING) {
+#pragma unroll
+        for (int u = 0; u < GV_RING; ++u) {
+            const int t = t0 + u;
+            int jn = j + 1, prn = pr;
+            if (jn == nchunk) { jn = 0; ++prn; }
+            float xn[MR][8];
+            load_x(xn, jn);
+#pragma unroll
+            for (int r = 0; r < GV_NR; ++r) {
+                const uint4 wv = ring[u][r];
+                const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float w = splitee::bf16_bits_to_f32((e & 1) ? (wd[e / 2] >> 16) : (wd[e / 2] & 0xFFFFu));
+#pragma unroll
+                    for (int m = 0; m < MR; ++m) acc[m][r] = fmaf(xc[m][e], w, acc[m][r]);
+                }
+                const int n = n0 + prr * GV_NR + r, k = 512 * jr + 8 * lane;
+                const bool ok = t + GV_RING < units_w && n < N && k < K;
+                ring[u][r] = load16(rw, ok ? (uint32_t)(((int64_t)n * ldw + k) * 2) : OOB);
+            }
+            if (++jr == nchunk) { jr = 0; ++prr; }
+            // last chunk of a row pair: wave sums, unmask, store, restart
+            if (j == nchunk - 1 && t < units_w) {
+#pragma unroll
+                for (int m = 0; m < MR; ++m)
+#pragma unroll
+                    for (int r = 0; r < GV_NR; ++r) {
+                        const float y = gv_wave_sum(acc[m][r]);
+                        const int64_t col = n0 + pr * GV_NR + r;
+                        if (lane == 0 && col < N) Out[(int64_t)m * ldo + col] = C ? y - C[(int64_t)m * ldc + col] : y;
+                        acc[m][r] = 0.f;
+                    }
+            }
+#pragma unroll
+            for (int m = 0; m < MR; ++m)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xc[m][e] = xn[m][e];
+            j = jn;
+            pr = prn;
+        }
+    }
+}
+
 // ------------------------------------------------------------ host planning
 
 struct Plan {
@@ -1020,6 +1207,26 @@ Plan plan_skinny(int64_t M, int64_t N, int64_t K, int prec)
     return p;
 }
 
+// M <= GV_MMAX: the GEMV kernel; x~ of all K sits in LDS.
+template <bool MASK>
+int launch_gemv(const SkSrc& src, int prec, const void* W, int64_t ldw, const float* C, int64_t ldc, float* Out,
+                int64_t ldo, int64_t M, int64_t N, int64_t K, hipStream_t s)
+{
+    const size_t lds = (size_t)M * (size_t)K * 4;
+    if (lds > 160 * 1024) return SPLITEE_ERR_UNSUPPORTED;
+    // row pairs per wave: the fewest that keep the grid within two workgroups per CU
+    const int64_t pairs = (N + GV_NR - 1) / GV_NR;
+    const int ppw = (int)((pairs + GV_MAX_WGS * GV_WAVES - 1) / (GV_MAX_WGS * GV_WAVES));
+    const int64_t waves = (pairs + ppw - 1) / ppw;
+    dim3 grid((unsigned)((waves + GV_WAVES - 1) / GV_WAVES));
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+#define GV_LAUNCH(NP, MR) hipLaunchKernelGGL((gemv_kernel<NP, MASK, MR>), grid, dim3(GV_WAVES * WAVE), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)N, (int)K, ppw)
+    if (prec == SPLITEE_PREC_BF16) { if (M == 1) GV_LAUNCH(1, 1); else GV_LAUNCH(1, 2); }
+    else { if (M == 1) GV_LAUNCH(3, 1); else GV_LAUNCH(3, 2); }
+#undef GV_LAUNCH
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
+
 }  // namespace
 
 namespace splitee_host {
@@ -1113,6 +1320,8 @@ int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const v
     const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
     if ((npl - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
         return SPLITEE_ERR_UNSUPPORTED;
+    const SkSrc src{reinterpret_cast<const uint16_t*>(A), lda, pstride, nullptr, 0, nullptr, 0};
+    if (M <= GV_MMAX) return launch_gemv<false>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
     Plan p = plan_skinny(M, N, K, prec);
     const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
     if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
@@ -1120,7 +1329,6 @@ int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const v
     unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
     float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
     dim3 grid((unsigned)(p.ntiles * p.ksplit));
-    const SkSrc src{reinterpret_cast<const uint16_t*>(A), lda, pstride, nullptr, 0, nullptr, 0};
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
     if (prec == SPLITEE_PREC_BF16)
         hipLaunchKernelGGL((skinny_kernel<1, SK_RING, false>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
@@ -1141,6 +1349,8 @@ int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t 
         N * ldw * 2 >= (int64_t(1) << 31))
         return SPLITEE_ERR_UNSUPPORTED;
     const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
+    const SkSrc src{nullptr, 0, 0, X, ldx, eta, ld_eta};
+    if (M <= GV_MMAX) return launch_gemv<true>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
     Plan p = plan_skinny(M, N, K, prec);
     const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
     if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
@@ -1148,7 +1358,6 @@ int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t 
     unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
     float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
     dim3 grid((unsigned)(p.ntiles * p.ksplit));
-    const SkSrc src{nullptr, 0, 0, X, ldx, eta, ld_eta};
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
     if (prec == SPLITEE_PREC_BF16)
         hipLaunchKernelGGL((skinny_kernel<1, SK_RING, true>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);

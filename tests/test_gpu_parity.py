@@ -257,7 +257,7 @@ def test_fused_skinny_decode(prec, M, N, K):
 
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
-@pytest.mark.parametrize("M", [1, 3, 16])
+@pytest.mark.parametrize("M", [1, 2, 3, 16])
 @pytest.mark.parametrize("N,K,xpad", [(6144, 2560, 0), (200, 9728, 8), (40, 264, 0)])
 def test_fused_precomputed_mask_is_the_two_launch_path(prec, M, N, K, xpad):
     # decode with a precomputed mask forms fl32(X + eta) inside the GEMM: bit for
