@@ -416,6 +416,12 @@ def main():
     pname = {v: k for k, v in sp.PRECS.items()}[prec]
     names = [p.name for p in path.projs]
     traffic = measured_traffic(args.workload, pname, names)
+    # bf16x3 issues three MFMA passes per algorithmic flop (the exact split of the masked input)
+    planes = 3 if prec == sp.SPLITEE_PREC_BF16X3 else 1
+    if prec != sp.SPLITEE_PREC_F32 and not path.decode:
+        issued = planes * sum(gflops) / (gemm_us * 1e-6) / 1e12
+        roofline.update({"mfma_issued_tflops": round(issued, 1),
+                         "mfma_issued_frac": round(issued / BF16_PEAK_TFS, 4), "mfma_passes": planes})
     roofline.update({"traffic": None if traffic is None else int(sum(traffic.values())),
                      "traffic_per_launch": traffic and {k: int(v) for k, v in traffic.items()},
                      "kernel": ("mask + GEMM + unmask (one launch per projection group, on the masks "
