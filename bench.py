@@ -22,7 +22,11 @@ weight set back to back in one HIP graph, bracketed by HIP events on the stream
 they run on; ``traffic`` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
 summary of the workload when the kernel sources still match it, else null),
 ``cpu_baseline`` (the CPU oracle on a bounded sample of the same workload),
-``modes`` (other precision modes), ``correction_ms`` (offline precompute).
+``modes`` (other precision modes), ``correction_ms`` (offline precompute),
+``noise_scale`` (the offline noise-scale step of the same model: spectral norms
+of W_val, W_up and W_gate by the power method, the sensitivity bounds of
+Theorems 1-3 from them, and the time of one power-method round against the
+HBM roofline of reading W once).
 """
 import argparse
 import json
@@ -53,6 +57,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-noise-scale", action="store_true", help="skip the noise-scale leg")
+    ap.add_argument("--noise-scale-only", action="store_true", help="run only the noise-scale leg")
+    ap.add_argument("--power-iters", type=int, default=300)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (HBM counter calibration) and exit")
     ap.add_argument("--counter-launches", type=int, default=0,
@@ -373,6 +380,58 @@ def copy_probe(mib):
     print(json.dumps({"copy_probe_mib": mib, "read_bytes": n * 4, "write_bytes": n * 4}), flush=True)
 
 
+def noise_scale_leg(torch, sp, WL, workload, iters):
+    """Offline noise scale of one layer of the workload's model (random-init weights,
+    normalisation parameters from workloads.gen_norm): ||W||_2 by the power method,
+    Delta of Theorems 1-3, and the time of one round (difference of two runs of
+    different lengths, HIP events on the stream the kernels run on)."""
+    model = WL.QWEN3_4B if workload.startswith("qwen") else WL.LLAMA_3B
+    d = model.hidden
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    mats = {"w_val": (model.kv_dim, d), "w_up": (model.ff, d), "w_gate": (model.ff, d),
+            "w_down": (d, model.ff)}
+    Ws = {k: (torch.randn(s, generator=g, device="cuda") * 0.02).to(torch.bfloat16) for k, s in mats.items()}
+    sig = {k: sp.spectral_norm(W, iters, 0, WL.stream_id(0, 16 + i)) for i, (k, W) in enumerate(Ws.items())}
+    alpha, beta = (torch.from_numpy(a).cuda() for a in WL.gen_norm(d))
+    delta = {"ln": sp.sensitivity(sp.SPLITEE_BOUND_LN, alpha),
+             "att": sp.sensitivity(sp.SPLITEE_BOUND_ATT, alpha, w_norm_a=sig["w_val"]),
+             "act": sp.sensitivity(sp.SPLITEE_BOUND_ACT, alpha, beta, sig["w_up"], sig["w_gate"])}
+    stream = torch.cuda.current_stream()
+
+    def timed(W, n):
+        nbytes = sp.splitee_spectral_norm_workspace_bytes(W.shape[0], W.shape[1], n)
+        ws = torch.empty(nbytes + 256, dtype=torch.uint8, device="cuda")
+        ws = ws[(-ws.data_ptr()) % 256:][:nbytes]
+        best = float("inf")
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            sp.splitee_spectral_norm(W, sp.SPLITEE_BF16, W.shape[1], W.shape[0], W.shape[1], n, 0, 0, ws,
+                                     nbytes, stream=stream)
+            b.record(stream)
+            b.synchronize()
+            best = min(best, a.elapsed_time(b) * 1e3)
+        return best
+
+    round_us, gbs = {}, {}
+    for k, W in Ws.items():
+        timed(W, 5)
+        t = (timed(W, 60) - timed(W, 10)) / 50.0
+        round_us[k] = round(t, 2)
+        gbs[k] = round(W.numel() * 2 / (t * 1e-6) / 1e9, 1)
+    big = max(Ws, key=lambda k: Ws[k].numel())
+    return {"model": model.name, "iters": iters, "sigma": {k: round(v, 6) for k, v in sig.items()},
+            "delta": {k: float("%.6g" % v) for k, v in delta.items()},
+            "round_us": round_us,
+            "roofline": {"bound": "hbm", "kernel": "power-method round (pi_round + pi_reduce), %s %dx%d bf16"
+                         % ((big,) + tuple(Ws[big].shape)),
+                         "achieved": gbs[big], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(gbs[big] / HBM_PEAK_GBS, 4),
+                         "bytes_per_round": {k: int(W.numel() * 2) for k, W in Ws.items()},
+                         "achieved_per_matrix": gbs}}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -396,6 +455,10 @@ def main():
         prec = sp.SPLITEE_PREC_F32
     if args.counter_launches:
         counter_launches(torch, sp, WL, args, prec)
+        return
+    if args.noise_scale_only:
+        print(json.dumps({"noise_scale": noise_scale_leg(torch, sp, WL, args.workload, args.power_iters)}),
+              flush=True)
         return
     path, ms, per_proj_us = run_mode(torch, sp, WL, args.workload, prec, args, args.steps, args.warmup)
     flops = path.flops()
@@ -455,6 +518,8 @@ def main():
         "correction_ms": round(path.correction_ms, 4),
         "modes": modes,
     }
+    if not args.no_noise_scale:
+        out["noise_scale"] = noise_scale_leg(torch, sp, WL, args.workload, args.power_iters)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(WL, args.cpu_seconds, path.projs, path.M, path.w_dtype)
     print(json.dumps(out), flush=True)

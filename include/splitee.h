@@ -241,6 +241,78 @@ int splitee_correction(float* C, int64_t ldc, const void* W, int w_type, int64_t
 int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_slow, float* out,
                             void* stream);
 
+/*
+ * Noise scale (Prop. 2: the Gaussian mask has standard deviation Delta f / eps per
+ * coordinate) from the global sensitivity bounds of Sec. "Global Sensitivity
+ * Analysis".  d is the model width; alpha, beta the scale and shift of the layer
+ * normalisation that precedes the bounded component.
+ *   SPLITEE_BOUND_LN   Theorem 1: 2 sqrt(d) ||alpha||_4
+ *                      (inputs of QKV, Gate / Up and the LM head)
+ *   SPLITEE_BOUND_ATT  Theorem 2: 2 sqrt(d) ||W_val||_2 ||alpha||_4       (input of O)
+ *   SPLITEE_BOUND_ACT  Theorem 3: 2 sqrt(d) (sqrt(d) ||alpha||_4 + ||beta||_2)^2
+ *                      ||W_up||_2 ||W_gate||_2                          (input of Down)
+ */
+typedef enum { SPLITEE_BOUND_LN = 0, SPLITEE_BOUND_ATT = 1, SPLITEE_BOUND_ACT = 2 } splitee_bound;
+
+/* Workspace bytes needed by splitee_spectral_norm for an N x K matrix and `iters`
+ * rounds; 0 on invalid arguments. */
+size_t splitee_spectral_norm_workspace_bytes(int64_t N, int64_t K, int iters);
+
+/*
+ * Spectral norm ||W||_2, the largest singular value (the matrix norm whose
+ * consistency, Eq. matrix-norm, the proofs of Theorems 2 and 3 use), by the power
+ * method on W^T W: from v_0 = g / ||g||, each round forms u = W v, sigma = ||u||,
+ * z = W^T u and v = z / ||z||.  g is the standard Gaussian row 0 of noise stream
+ * (seed, stream_id), i.e. what splitee_noise_gen(g, K, 1, K, SPLITEE_MECH_GAUSSIAN,
+ * 1, 1, seed, stream_id, 0, stream) writes.  sigma never exceeds ||W||_2 in exact
+ * arithmetic and rises towards it at a rate set by the gap between the two largest
+ * singular values; the caller chooses iters.
+ *   W          N x K, w_type (splitee_dtype), leading dimension ldw >= K, row-major,
+ *              16-byte aligned with a 16-byte row pitch; read only
+ *   N, K       N >= 0, 0 <= K <= 16384, K % 8 == 0 (K above 16384:
+ *              SPLITEE_ERR_UNSUPPORTED); N == 0 or K == 0 gives sigma = 0 and launches
+ *              nothing
+ *   iters      1 <= iters <= 1048576
+ *   sigma      host, receives sigma of the last round
+ *   history    host array of iters entries or NULL; receives sigma of every round
+ *   workspace  device, >= splitee_spectral_norm_workspace_bytes(N, K, iters) bytes,
+ *              256-byte aligned; no initial contents needed
+ * Products accumulate in float32, squared norms in binary64.  The call
+ * synchronises `stream` before it returns.
+ */
+int splitee_spectral_norm(const void* W, int w_type, int64_t ldw, int64_t N, int64_t K, int iters,
+                          uint64_t seed, uint64_t stream_id, double* sigma, double* history,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by splitee_sensitivity. */
+size_t splitee_sensitivity_workspace_bytes(void);
+
+/*
+ * Sensitivity bound Delta f of one component (splitee_bound above).
+ *   d          model width, >= 1
+ *   alpha      device, d float32 (the normalisation scale); required
+ *   beta       device, d float32 (the normalisation shift) or NULL for beta = 0; read
+ *              only by SPLITEE_BOUND_ACT
+ *   w_norm_a   ||W_val||_2 (ATT) or ||W_up||_2 (ACT); unused for LN; finite, >= 0
+ *   w_norm_b   ||W_gate||_2 (ACT); unused otherwise; finite, >= 0
+ *   delta      host, receives the bound
+ *   workspace  device, >= splitee_sensitivity_workspace_bytes() bytes, 256-byte aligned
+ * The vector norms are reduced on the GPU in binary64 (sum of alpha^4, sum of beta^2);
+ * the bound is assembled from them in binary64.  The call synchronises `stream`.
+ */
+int splitee_sensitivity(int bound, int64_t d, const float* alpha, const float* beta, double w_norm_a,
+                        double w_norm_b, double* delta, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/*
+ * Per-token privacy budget: n releases that are each eps-GDP compose to
+ * sqrt(n) eps-GDP (Prop. "Sequential Composition"), so a prompt of n tokens within a
+ * total budget eps_total takes eps = eps_total / sqrt(n) per token (the EPN
+ * configuration of the experiments).  eps_total > 0 and finite, n >= 1; *eps is written on
+ * success.  Host only.
+ */
+int splitee_eps_per_token(double eps_total, int64_t n, double* eps);
+
 #ifdef __cplusplus
 }
 #endif

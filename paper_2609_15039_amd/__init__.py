@@ -20,13 +20,15 @@ SPLITEE_F32, SPLITEE_BF16 = 0, 1
 SPLITEE_PREC_F32, SPLITEE_PREC_BF16, SPLITEE_PREC_BF16X3 = 0, 1, 2
 MECHS = {"laplace": SPLITEE_MECH_LAPLACE, "gaussian": SPLITEE_MECH_GAUSSIAN, "none": SPLITEE_MECH_NONE}
 PRECS = {"f32": SPLITEE_PREC_F32, "bf16": SPLITEE_PREC_BF16, "bf16x3": SPLITEE_PREC_BF16X3}
+SPLITEE_BOUND_LN, SPLITEE_BOUND_ATT, SPLITEE_BOUND_ACT = 0, 1, 2
 
 EXPORTED = [
     "splitee_abi_version", "splitee_status_string", "splitee_noise_gen", "splitee_mask",
     "splitee_masked_linear", "splitee_unmask", "splitee_fused_workspace_bytes",
     "splitee_masked_linear_fused", "splitee_correction", "splitee_transform_probe",
     "splitee_noise_mask", "splitee_gemm_workspace_bytes", "splitee_masked_linear_unmask",
-    "splitee_noise_gen_multi",
+    "splitee_noise_gen_multi", "splitee_spectral_norm_workspace_bytes", "splitee_spectral_norm",
+    "splitee_sensitivity_workspace_bytes", "splitee_sensitivity", "splitee_eps_per_token",
 ]
 
 
@@ -67,6 +69,11 @@ def load():
         "splitee_masked_linear_unmask": (I, [P, I, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, P,
                                              SZ, P]),
         "splitee_noise_gen_multi": (I, [P, P, P, P, I, I, P, U64, I64, I, D, D, U64, U64, P]),
+        "splitee_spectral_norm_workspace_bytes": (SZ, [I64, I64, I]),
+        "splitee_spectral_norm": (I, [P, I, I64, I64, I64, I, U64, U64, P, P, P, SZ, P]),
+        "splitee_sensitivity_workspace_bytes": (SZ, []),
+        "splitee_sensitivity": (I, [I, I64, P, P, D, D, P, P, SZ, P]),
+        "splitee_eps_per_token": (I, [D, I64, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -206,7 +213,65 @@ def splitee_masked_linear_unmask(Xt, in_prec, ldxt, W, w_type, ldw, C, ldc, Y, l
         _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
+def splitee_spectral_norm_workspace_bytes(N, K, iters):
+    return load().splitee_spectral_norm_workspace_bytes(N, K, iters)
+
+
+def splitee_spectral_norm(W, w_type, ldw, N, K, iters, seed, stream_id, workspace, workspace_bytes,
+                          history=False, stream=None):
+    """Returns sigma of the last round, or (sigma, [sigma of every round]) with history."""
+    sigma = ctypes.c_double()
+    hist = (ctypes.c_double * iters)() if history and iters > 0 else None
+    _check("splitee_spectral_norm", load().splitee_spectral_norm(
+        _ptr(W), w_type, ldw, N, K, iters, seed, stream_id, ctypes.byref(sigma),
+        ctypes.cast(hist, ctypes.c_void_p) if hist is not None else None, _ptr(workspace), workspace_bytes,
+        _stream(stream)))
+    return (sigma.value, list(hist) if hist is not None else []) if history else sigma.value
+
+
+def splitee_sensitivity_workspace_bytes():
+    return load().splitee_sensitivity_workspace_bytes()
+
+
+def splitee_sensitivity(bound, d, alpha, beta, w_norm_a, w_norm_b, workspace, workspace_bytes, stream=None):
+    """Returns the bound Delta f."""
+    delta = ctypes.c_double()
+    _check("splitee_sensitivity", load().splitee_sensitivity(
+        bound, d, _ptr(alpha), _ptr(beta), w_norm_a, w_norm_b, ctypes.byref(delta), _ptr(workspace),
+        workspace_bytes, _stream(stream)))
+    return delta.value
+
+
+def splitee_eps_per_token(eps_total, n):
+    eps = ctypes.c_double()
+    _check("splitee_eps_per_token", load().splitee_eps_per_token(eps_total, n, ctypes.byref(eps)))
+    return eps.value
+
+
 # ------------------------------------------------- tensor-level conveniences
+
+def _aligned_bytes(nbytes, device):
+    buf = torch.empty(max(nbytes, 1) + 256, dtype=torch.uint8, device=device)
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + max(nbytes, 1)]
+
+
+def spectral_norm(W, iters, seed, stream_id, history=False, ws=None):
+    """||W||_2 of a row-major N x K tensor by the power method (see splitee_spectral_norm)."""
+    N, K = W.shape
+    nbytes = splitee_spectral_norm_workspace_bytes(N, K, iters)
+    if ws is None:
+        ws = _aligned_bytes(nbytes, W.device)
+    return splitee_spectral_norm(W, _wtype(W), W.stride(0), N, K, iters, seed, stream_id, ws, nbytes,
+                                 history=history)
+
+
+def sensitivity(bound, alpha, beta=None, w_norm_a=0.0, w_norm_b=0.0):
+    """Delta f of Theorem 1 (LN), 2 (ATT) or 3 (ACT) for float32 device vectors."""
+    nbytes = splitee_sensitivity_workspace_bytes()
+    ws = _aligned_bytes(nbytes, alpha.device)
+    return splitee_sensitivity(bound, alpha.numel(), alpha, beta, w_norm_a, w_norm_b, ws, nbytes)
+
 
 def workspace(M, N, K, prec, device="cuda", gemm_only=False):
     """A zeroed, 256-byte aligned workspace for the fused call / correction (or, with

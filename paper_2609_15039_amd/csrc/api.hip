@@ -12,6 +12,7 @@ size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec);
 namespace {
 
 constexpr int64_t MAX_DIM = int64_t(1) << 30;
+constexpr int MAX_POWER_ITERS = 1 << 20;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -314,6 +315,73 @@ int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_
     if (n == 0) return SPLITEE_OK;
     if (!words || !out) return SPLITEE_ERR_ARG;
     return splitee_host::launch_transform_probe(words, n, fn, force_slow, out, as_stream(stream));
+}
+
+size_t splitee_spectral_norm_workspace_bytes(int64_t N, int64_t K, int iters)
+{
+    if (!dims_ok(0, N, K) || iters < 1 || iters > MAX_POWER_ITERS || K > splitee_host::spectral_max_k()) return 0;
+    return splitee_host::spectral_workspace_bytes(N, K, iters);
+}
+
+int splitee_spectral_norm(const void* W, int w_type, int64_t ldw, int64_t N, int64_t K, int iters,
+                          uint64_t seed, uint64_t stream_id, double* sigma, double* history,
+                          void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (!valid_dtype(w_type)) return SPLITEE_ERR_DTYPE;
+    if (iters < 1 || iters > MAX_POWER_ITERS || !sigma) return SPLITEE_ERR_ARG;
+    if (!dims_ok(0, N, K) || K % 8 != 0 || ldw < K) return SPLITEE_ERR_SHAPE;
+    if (K > splitee_host::spectral_max_k()) return SPLITEE_ERR_UNSUPPORTED;
+    if (N == 0 || K == 0) {
+        *sigma = 0.0;
+        if (history)
+            for (int i = 0; i < iters; ++i) history[i] = 0.0;
+        return SPLITEE_OK;
+    }
+    if (!W) return SPLITEE_ERR_ARG;
+    if (!aligned16(W) || !pitch16(ldw, w_type == SPLITEE_F32 ? 4 : 2)) return SPLITEE_ERR_ALIGN;
+    if (!workspace || workspace_bytes < splitee_host::spectral_workspace_bytes(N, K, iters))
+        return SPLITEE_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return SPLITEE_ERR_ALIGN;
+    return splitee_host::launch_spectral_norm(W, w_type, ldw, N, K, iters, seed, stream_id, sigma, history,
+                                              workspace, as_stream(stream));
+}
+
+size_t splitee_sensitivity_workspace_bytes(void) { return 256; }
+
+int splitee_sensitivity(int bound, int64_t d, const float* alpha, const float* beta, double w_norm_a,
+                        double w_norm_b, double* delta, void* workspace, size_t workspace_bytes,
+                        void* stream)
+{
+    if (bound != SPLITEE_BOUND_LN && bound != SPLITEE_BOUND_ATT && bound != SPLITEE_BOUND_ACT)
+        return SPLITEE_ERR_ARG;
+    if (d < 1 || d > MAX_DIM) return SPLITEE_ERR_SHAPE;
+    if (!alpha || !delta) return SPLITEE_ERR_ARG;
+    const bool uses_a = bound != SPLITEE_BOUND_LN, uses_b = bound == SPLITEE_BOUND_ACT;
+    if (uses_a && !(w_norm_a >= 0.0 && isfinite(w_norm_a))) return SPLITEE_ERR_ARG;
+    if (uses_b && !(w_norm_b >= 0.0 && isfinite(w_norm_b))) return SPLITEE_ERR_ARG;
+    if (!workspace || workspace_bytes < splitee_sensitivity_workspace_bytes()) return SPLITEE_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return SPLITEE_ERR_ALIGN;
+    double sums[2];
+    const int rc = splitee_host::launch_vec_norms(alpha, uses_b ? beta : nullptr, d,
+                                                  reinterpret_cast<double*>(workspace), sums, as_stream(stream));
+    if (rc) return rc;
+    const double n4 = pow(sums[0], 0.25), b2 = sqrt(sums[1]), sd = sqrt((double)d);
+    if (bound == SPLITEE_BOUND_LN)
+        *delta = 2.0 * sd * n4;  // Theorem 1
+    else if (bound == SPLITEE_BOUND_ATT)
+        *delta = 2.0 * sd * w_norm_a * n4;  // Theorem 2
+    else {
+        const double t = sd * n4 + b2;  // Theorem 3
+        *delta = 2.0 * sd * (t * t) * w_norm_a * w_norm_b;
+    }
+    return SPLITEE_OK;
+}
+
+int splitee_eps_per_token(double eps_total, int64_t n, double* eps)
+{
+    if (!(eps_total > 0.0) || !isfinite(eps_total) || n < 1 || !eps) return SPLITEE_ERR_ARG;
+    *eps = eps_total / sqrt((double)n);
+    return SPLITEE_OK;
 }
 
 }  // extern "C"

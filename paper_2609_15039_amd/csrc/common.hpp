@@ -77,4 +77,11 @@ size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
 int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
                   int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,
                   int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+// Power method for ||W||_2 and the vector norms of the sensitivity bounds.
+size_t spectral_workspace_bytes(int64_t N, int64_t K, int iters);
+int spectral_max_k();
+int launch_spectral_norm(const void* W, int w_type, int64_t ldw, int64_t N, int64_t K, int iters, uint64_t seed,
+                         uint64_t sid, double* sigma, double* history, void* ws, hipStream_t s);
+int launch_vec_norms(const float* alpha, const float* beta, int64_t d, double* out_dev, double* out_host,
+                     hipStream_t s);
 }  // namespace splitee_host

@@ -154,3 +154,69 @@ def test_workspace_sizes(lib):
 def test_transform_probe_validation(lib):
     assert lib.splitee_transform_probe(P, 4, 4, 0, P, None) == ARG
     assert lib.splitee_transform_probe(P, 0, 0, 0, P, None) == OK
+
+
+def spectral(lib, W=P, wt=BF16, ldw=8, N=4, K=8, iters=3, sigma=True, hist=None, ws=256, wsb=1 << 20):
+    s = ctypes.c_double(-1.0)
+    rc = lib.splitee_spectral_norm(W, wt, ldw, N, K, iters, 0, 0, ctypes.byref(s) if sigma else None, hist, ws,
+                                   wsb, None)
+    return rc, s.value
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(wt=2), DTYPE), (dict(iters=0), ARG), (dict(iters=(1 << 20) + 1), ARG), (dict(sigma=False), ARG),
+    (dict(K=12, ldw=16), SHAPE), (dict(ldw=4), SHAPE), (dict(N=-1), SHAPE), (dict(K=-8), SHAPE),
+    (dict(W=None), ARG), (dict(W=8), ALIGN), (dict(ldw=12), ALIGN), (dict(wt=F32, ldw=10, K=8), ALIGN),
+    (dict(ws=None), WS), (dict(wsb=16), WS), (dict(ws=16), ALIGN)])
+def test_spectral_norm_validation(lib, kw, code):
+    assert spectral(lib, **kw)[0] == code
+
+
+def test_spectral_norm_of_empty_matrix_is_zero(lib):
+    hist = (ctypes.c_double * 3)(7.0, 7.0, 7.0)
+    for N, K in ((0, 8), (4, 0)):
+        rc, s = spectral(lib, N=N, K=K, hist=ctypes.cast(hist, ctypes.c_void_p), ws=None, wsb=0)
+        assert (rc, s, list(hist)) == (OK, 0.0, [0.0, 0.0, 0.0])
+
+
+def test_spectral_norm_workspace_size(lib):
+    q = lib.splitee_spectral_norm_workspace_bytes
+    assert q(8, 8, 0) == 0 and q(-1, 8, 1) == 0
+    # partial rows (one per 16 rows of W) dominate: float32 per column
+    assert q(3072, 3072, 50) >= (3072 // 16) * 3072 * 4
+    assert q(3072, 3072, 50) % 256 == 0
+    assert q(3073, 3072, 50) > q(3072, 3072, 50)
+
+
+def sens(lib, bound=0, d=8, alpha=P, beta=None, a=1.0, b=1.0, delta=True, ws=256, wsb=256):
+    out = ctypes.c_double(-1.0)
+    return lib.splitee_sensitivity(bound, d, alpha, beta, a, b, ctypes.byref(out) if delta else None, ws, wsb,
+                                   None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bound=3), ARG), (dict(bound=-1), ARG), (dict(d=0), SHAPE), (dict(alpha=None), ARG),
+    (dict(delta=False), ARG), (dict(bound=1, a=-1.0), ARG), (dict(bound=1, a=math.inf), ARG),
+    (dict(bound=2, b=math.nan), ARG), (dict(ws=None), WS), (dict(wsb=8), WS), (dict(ws=16), ALIGN)])
+def test_sensitivity_validation(lib, kw, code):
+    assert sens(lib, **kw) == code
+
+
+def test_sensitivity_ignores_norms_it_does_not_use(lib):
+    # LN reads neither matrix norm and ATT not the second: invalid values there pass validation
+    # (workspace too small keeps the call from launching)
+    assert sens(lib, bound=0, a=math.nan, b=-1.0, wsb=8) == WS
+    assert sens(lib, bound=1, b=math.nan, wsb=8) == WS
+
+
+@pytest.mark.parametrize("eps,n", [(1.0, 1), (1.0, 128), (4.0, 512), (0.25, 10 ** 9)])
+def test_eps_per_token_matches_the_oracle(lib, eps, n):
+    from oracle import sensitivity as S
+    assert sp.splitee_eps_per_token(eps, n) == S.eps_per_token(eps, n)
+
+
+@pytest.mark.parametrize("eps,n", [(0.0, 4), (-1.0, 4), (math.inf, 4), (math.nan, 4), (1.0, 0), (1.0, -3)])
+def test_eps_per_token_validation(lib, eps, n):
+    out = ctypes.c_double()
+    assert lib.splitee_eps_per_token(eps, n, ctypes.byref(out)) == ARG
+    assert lib.splitee_eps_per_token(1.0, 4, None) == ARG

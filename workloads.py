@@ -11,6 +11,8 @@ available; these stand in for them):
   W ~ N(0, 0.02^2) drawn in float32, then rounded to bfloat16 by torch
     (float32 kept for the small float32 case); numpy PCG64, seed 2 + layer
   noise stream: seed 0, stream_id = (layer << 8) | group, row0 = 0 for prefill.
+  normalisation scale alpha ~ N(1, 0.1^2), shift beta ~ N(0, 0.02^2), float32, d wide
+    (stand-ins for trained values; alpha = 1, beta = 0 is the untrained layer)
 """
 from dataclasses import dataclass, field
 from typing import List
@@ -99,6 +101,14 @@ def gen_w(N: int, K: int, seed: int = 2, std: float = 0.02, dtype: str = "bf16")
         return w
     import torch
     return torch.from_numpy(w).to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def gen_norm(d: int, seed: int = 3, scale_std: float = 0.1, shift_std: float = 0.02):
+    """Normalisation parameters (alpha, beta), float32, d wide."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    alpha = (1.0 + scale_std * g.standard_normal(d)).astype(np.float32)
+    beta = (shift_std * g.standard_normal(d)).astype(np.float32)
+    return alpha, beta
 
 
 def gen_int(shape, lo: int, hi: int, seed: int) -> np.ndarray:
