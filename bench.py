@@ -71,7 +71,9 @@ def parse():
 
 
 WORKLOADS = ["llama3b-layer-m128", "single-fp32-m32", "llama3b-28l-m512", "qwen3-4b-36l-m1024",
-             "qwen3-4b-decode-m1", "qwen3-4b-decode-m4", "qwen3-4b-decode-m16", "qwen3-4b-decode-m64"]
+             "qwen3-4b-decode-m1", "qwen3-4b-decode-m4", "qwen3-4b-decode-m16", "qwen3-4b-decode-m64",
+             "llama3b-lmhead-m1", "llama3b-lmhead-m15", "llama3b-lmhead-m128",
+             "qwen3-4b-lmhead-m1", "qwen3-4b-lmhead-m15"]
 DECODE_POS = 1024  # decode position t: rows [t, t+M) of the 2048-position correction bank
 
 
@@ -89,6 +91,13 @@ def workload_spec(WL, name):
     if name.startswith("qwen3-4b-decode-m"):
         m = int(name.rsplit("m", 1)[1])
         return WL.QWEN3_4B.projections(), m, WL.QWEN3_4B.layers, 1, "bf16", 2048, DECODE_POS
+    if "-lmhead-m" in name:
+        # the vocabulary projection alone (788 / 778 MB of bf16 W, past the MALL by itself):
+        # decode sizes read their correction rows from a 2048-position bank
+        model = WL.QWEN3_4B if name.startswith("qwen") else WL.LLAMA_3B
+        m = int(name.rsplit("m", 1)[1])
+        bank, row0 = (2048, DECODE_POS) if m <= 16 else (0, 0)
+        return [model.lm_head()], m, 1, 1, "bf16", bank, row0
     raise ValueError(name)
 
 
@@ -106,7 +115,7 @@ class Path:
         self.prec, self.mech, self.delta, self.eps = prec, mech, delta, eps
         (self.projs, self.M, self.layers_per_step, nsets, self.w_dtype, bank_rows,
          self.row0) = workload_spec(WL, name)
-        if self.layers_per_step == 1 and weight_sets:
+        if self.layers_per_step == 1 and weight_sets and nsets > 1:
             nsets = weight_sets
         self.nsets = nsets if self.layers_per_step == 1 else 1
         nlayers = self.layers_per_step * self.nsets

@@ -38,6 +38,12 @@ class ModelShape:
     q_dim: int
     kv_dim: int
     ff: int
+    vocab: int
+
+    def lm_head(self) -> Projection:
+        """The vocabulary projection after the final normalisation (offloaded too,
+        Sec. "Inference Models"); its own noise group."""
+        return Projection("lm_head", self.hidden, self.vocab, 4)
 
     def projections(self) -> List[Projection]:
         return [
@@ -49,9 +55,10 @@ class ModelShape:
 
 
 # Sec. "Inference Models": Llama-3.2-3B (28 layers, d 3072, d_ff 8192, 24 q / 8 kv
-# heads of 128) and Qwen3-4B (36 layers, d 2560, q 4096, k/v 1024, d_ff 9728).
-LLAMA_3B = ModelShape("llama-3.2-3b", 28, 3072, 3072, 1024, 8192)
-QWEN3_4B = ModelShape("qwen3-4b", 36, 2560, 4096, 1024, 9728)
+# heads of 128, vocabulary 128256) and Qwen3-4B (36 layers, d 2560, q 4096, k/v 1024,
+# d_ff 9728, vocabulary 151936).
+LLAMA_3B = ModelShape("llama-3.2-3b", 28, 3072, 3072, 1024, 8192, 128256)
+QWEN3_4B = ModelShape("qwen3-4b", 36, 2560, 4096, 1024, 9728, 151936)
 
 
 def stream_id(layer: int, group: int) -> int:
