@@ -23,6 +23,8 @@ they run on; ``traffic`` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
 summary of the workload when the kernel sources still match it, else null),
 ``cpu_baseline`` (the CPU oracle on a bounded sample of the same workload),
 ``modes`` (other precision modes), ``correction_ms`` (offline precompute),
+``noise_bank`` (one layer's correction banks for 2048 positions: created from the
+GPU corrections into files, then loaded as decode steps and as one batch),
 ``noise_scale`` (the offline noise-scale step of the same model: spectral norms
 of W_val, W_up and W_gate by the power method, the sensitivity bounds of
 Theorems 1-3 from them, and the time of one power-method round against the
@@ -60,6 +62,8 @@ def parse():
     ap.add_argument("--no-noise-scale", action="store_true", help="skip the noise-scale leg")
     ap.add_argument("--noise-scale-only", action="store_true", help="run only the noise-scale leg")
     ap.add_argument("--power-iters", type=int, default=300)
+    ap.add_argument("--no-noise-bank", action="store_true", help="skip the noise-bank leg")
+    ap.add_argument("--noise-bank-only", action="store_true", help="run only the noise-bank leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (HBM counter calibration) and exit")
     ap.add_argument("--counter-launches", type=int, default=0,
@@ -441,6 +445,56 @@ def noise_scale_leg(torch, sp, WL, workload, iters):
                          "achieved_per_matrix": gbs}}
 
 
+def noise_bank_leg(torch, sp, WL, workload, rows=2048):
+    """The noise bank of one layer of the workload's model (its projection groups, random-init
+    bf16 weights, corrections in BF16X3): create the banks for `rows` positions in a
+    temporary directory, then load them as decode steps (16 rows per group per step) and
+    as one batch of all rows.  Times are host wall-clock around synchronising calls."""
+    import shutil
+    import tempfile
+    model = WL.QWEN3_4B if workload.startswith("qwen") else WL.LLAMA_3B
+    projs = model.projections()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    Ws = [(torch.randn((p.N, p.K), generator=g, device="cuda") * 0.02).to(torch.bfloat16) for p in projs]
+    d = tempfile.mkdtemp(prefix="splitee-bank-")
+    try:
+        paths = [sp.splitee_bank_path(d, p.K, p.N, WL.stream_id(0, p.group)) for p in projs]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for p, W, path in zip(projs, Ws, paths):
+            sp.bank_create(path, W, p.K, sp.SPLITEE_MECH_GAUSSIAN, 1.0, 1.0, 0, WL.stream_id(0, p.group), 0, rows)
+        t_create = time.perf_counter() - t0
+        banks = [sp.splitee_bank_open(path) for path in paths]
+        infos = [sp.splitee_bank_info(b) for b in banks]
+        Cs = [torch.empty((rows, p.N), device="cuda") for p in projs]
+        steps = rows // 2 // 16
+        t0 = time.perf_counter()
+        for s in range(steps):
+            for b, C, p in zip(banks, Cs, projs):
+                sp.splitee_bank_load(b, 16, C[16 * s:], p.N, True)
+        t_steps = time.perf_counter() - t0
+        rest = rows - 16 * steps
+        t0 = time.perf_counter()
+        for b, C, p in zip(banks, Cs, projs):
+            sp.splitee_bank_load(b, rest, C[16 * steps:], p.N, True)
+        t_batch = time.perf_counter() - t0
+        for b in banks:
+            sp.splitee_bank_close(b)
+    finally:
+        shutil.rmtree(d, ignore_errors=True)
+    row_bytes = sum(4 * p.N for p in projs)
+    flops = sum(2.0 * 3 * rows * p.N * p.K for p in projs)  # three MFMA passes of the exact split
+    return {"model": model.name, "groups": [p.name for p in projs], "rows": rows,
+            "bytes_stored": int(sum(i["bytes_stored"] for i in infos)),
+            "bytes_with_masks": int(sum(i["bytes_with_masks"] for i in infos)),
+            "create_s": round(t_create, 3), "create_GBps": round(rows * row_bytes / t_create / 1e9, 3),
+            "create_correction_TFLOPs_issued": round(flops / t_create / 1e12, 2),
+            "decode_load_us_per_step": round(t_steps / steps * 1e6, 1),
+            "decode_load_GBps": round(steps * 16 * row_bytes / t_steps / 1e9, 3),
+            "batch_load_GBps": round(rest * row_bytes / t_batch / 1e9, 3)}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -464,6 +518,9 @@ def main():
         prec = sp.SPLITEE_PREC_F32
     if args.counter_launches:
         counter_launches(torch, sp, WL, args, prec)
+        return
+    if args.noise_bank_only:
+        print(json.dumps({"noise_bank": noise_bank_leg(torch, sp, WL, args.workload)}), flush=True)
         return
     if args.noise_scale_only:
         print(json.dumps({"noise_scale": noise_scale_leg(torch, sp, WL, args.workload, args.power_iters)}),
@@ -527,6 +584,8 @@ def main():
         "correction_ms": round(path.correction_ms, 4),
         "modes": modes,
     }
+    if not args.no_noise_bank:
+        out["noise_bank"] = noise_bank_leg(torch, sp, WL, args.workload)
     if not args.no_noise_scale:
         out["noise_scale"] = noise_scale_leg(torch, sp, WL, args.workload, args.power_iters)
     if not args.no_cpu_baseline:

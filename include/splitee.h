@@ -87,7 +87,11 @@ typedef enum {
     SPLITEE_ERR_ALIGN = -4,
     SPLITEE_ERR_UNSUPPORTED = -5,
     SPLITEE_ERR_HIP = -6,
-    SPLITEE_ERR_WORKSPACE = -7
+    SPLITEE_ERR_WORKSPACE = -7,
+    SPLITEE_ERR_IO = -8,
+    SPLITEE_ERR_EXHAUSTED = -9,
+    SPLITEE_ERR_FORMAT = -10,
+    SPLITEE_ERR_BUSY = -11
 } splitee_status;
 
 typedef enum { SPLITEE_MECH_LAPLACE = 0, SPLITEE_MECH_GAUSSIAN = 1, SPLITEE_MECH_NONE = 2 } splitee_mech;
@@ -312,6 +316,84 @@ int splitee_sensitivity(int bound, int64_t d, const float* alpha, const float* b
  * success.  Host only.
  */
 int splitee_eps_per_token(double eps_total, int64_t n, double* eps);
+
+/*
+ * Noise bank (Sec. "Precomputing the Mask and Noise Correction"): the corrections
+ * C = eta W^T of one projection group, precomputed for rows row0 .. row0 + rows - 1 of
+ * one noise stream, stored in a file, loaded per batch and handed out exactly once.
+ * The paper keeps a separate bank per offloaded component (QKV, O, Gate/Up, LM head)
+ * and indexes it by the input shape; here a bank is one (stream_id, K, N) and
+ * splitee_bank_path names its file in a bank directory.  The masks are not stored:
+ * the fused call regenerates eta from (seed, stream_id, row), so a bank takes
+ * rows x N x 4 bytes instead of rows x (K + N) x 4.
+ *
+ * A bank file has a 128-byte header (see csrc/bank.cpp) and rows x N float32.  Its
+ * single-use watermark `consumed` is written to the file and synced before the
+ * rows it covers are read; a row is never handed out twice, also across processes
+ * (one open handle per file at a time: a second open gets SPLITEE_ERR_BUSY).  Rows
+ * taken by a load that then fails are lost, not reissued.  Handles are not
+ * thread-safe.
+ */
+typedef struct splitee_bank splitee_bank;
+
+typedef struct {
+    int64_t K, N;                 /* mask width, correction width */
+    uint64_t seed, stream_id;     /* the noise stream */
+    int32_t mech, prec;           /* splitee_mech; splitee_prec the corrections were computed in */
+    double sensitivity, epsilon;  /* noise scale Delta / eps */
+    int64_t row0, rows;           /* stream rows row0 .. row0 + rows - 1 are stored */
+    int64_t consumed;             /* rows row0 .. row0 + consumed - 1 have been handed out */
+    int64_t bytes_stored;         /* file size: header + rows x N float32 */
+    int64_t bytes_with_masks;     /* the same bank storing the masks too: + rows x K float32 */
+} splitee_bank_info_t;
+
+/* Canonical file of the bank of (stream_id, K, N) in directory dir (the shape index):
+ * "<dir>/bank-s<stream_id, 16 hex digits>-k<K>-n<N>.spb", written to out (out_len
+ * bytes, NUL-terminated); SPLITEE_ERR_ARG if it does not fit. */
+int splitee_bank_path(const char* dir, int64_t K, int64_t N, uint64_t stream_id, char* out, size_t out_len);
+
+/* Device workspace bytes splitee_bank_create needs: the fused call's workspace for 256
+ * rows plus a 256 x N float32 staging block; 0 on invalid arguments. */
+size_t splitee_bank_workspace_bytes(int64_t K, int64_t N, int prec);
+
+/*
+ * Precompute and store a bank: C rows for stream rows row0 .. row0 + rows - 1, in
+ * blocks of 256 rows, each exactly what splitee_correction(C, N, W, ..., block rows,
+ * N, K, mech, sensitivity, epsilon, seed, stream_id, block row0, prec, ...) writes.
+ *   path        new file; an existing file is never overwritten (SPLITEE_ERR_IO)
+ *   W, w_type, ldw, K, N, mech, sensitivity, epsilon, seed, stream_id, prec
+ *               as for splitee_correction (prec F32 or BF16X3); N % 4 == 0
+ *   rows        >= 0 (0 writes an empty bank)
+ *   workspace   device, >= splitee_bank_workspace_bytes(K, N, prec) bytes, 256-byte
+ *               aligned, zeros at first use (left that way), as for the fused call
+ * The header is written last; a failed call removes the file.  Synchronises `stream`.
+ */
+int splitee_bank_create(const char* path, const void* W, int w_type, int64_t ldw, int64_t K, int64_t N, int mech,
+                        double sensitivity, double epsilon, uint64_t seed, uint64_t stream_id, uint64_t row0,
+                        int64_t rows, int prec, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Open a bank file: SPLITEE_ERR_IO if it cannot be opened, SPLITEE_ERR_BUSY if another
+ * handle holds it, SPLITEE_ERR_FORMAT if its header or size is inconsistent. */
+int splitee_bank_open(const char* path, splitee_bank** bank);
+
+/* The bank's parameters, watermark and storage accounting. Host only. */
+int splitee_bank_info(const splitee_bank* bank, splitee_bank_info_t* info);
+
+/*
+ * Load the next `rows` rows not yet handed out into C (rows x N float32, leading
+ * dimension ldc >= N; device memory if dst_device != 0, else host memory) and take
+ * them: *row0 receives their first stream row, to be passed as row0 to the fused call
+ * together with these C rows.  SPLITEE_ERR_EXHAUSTED if fewer rows remain (nothing
+ * taken).  rows == 0 only reports the next row.  Synchronises `stream` for a device
+ * destination, which goes through pinned host memory that the handle keeps (up to 256
+ * rows) until it is closed.  Every load syncs the watermark to the file, so loading a
+ * batch's rows at once costs far less than one load per decode step.
+ */
+int splitee_bank_load(splitee_bank* bank, int64_t rows, float* C, int64_t ldc, int dst_device, int64_t* row0,
+                      void* stream);
+
+/* Close the handle and free its pinned staging memory (the file and its watermark stay). */
+int splitee_bank_close(splitee_bank* bank);
 
 #ifdef __cplusplus
 }

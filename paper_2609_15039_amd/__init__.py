@@ -29,7 +29,22 @@ EXPORTED = [
     "splitee_noise_mask", "splitee_gemm_workspace_bytes", "splitee_masked_linear_unmask",
     "splitee_noise_gen_multi", "splitee_spectral_norm_workspace_bytes", "splitee_spectral_norm",
     "splitee_sensitivity_workspace_bytes", "splitee_sensitivity", "splitee_eps_per_token",
+    "splitee_bank_path", "splitee_bank_workspace_bytes", "splitee_bank_create", "splitee_bank_open",
+    "splitee_bank_info", "splitee_bank_load", "splitee_bank_close",
 ]
+SPLITEE_ERR_IO, SPLITEE_ERR_EXHAUSTED, SPLITEE_ERR_FORMAT, SPLITEE_ERR_BUSY = -8, -9, -10, -11
+
+
+class BankInfo(ctypes.Structure):
+    """splitee_bank_info_t"""
+    _fields_ = [("K", ctypes.c_int64), ("N", ctypes.c_int64), ("seed", ctypes.c_uint64),
+                ("stream_id", ctypes.c_uint64), ("mech", ctypes.c_int32), ("prec", ctypes.c_int32),
+                ("sensitivity", ctypes.c_double), ("epsilon", ctypes.c_double), ("row0", ctypes.c_int64),
+                ("rows", ctypes.c_int64), ("consumed", ctypes.c_int64), ("bytes_stored", ctypes.c_int64),
+                ("bytes_with_masks", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
 
 
 class SpliteeError(RuntimeError):
@@ -74,6 +89,14 @@ def load():
         "splitee_sensitivity_workspace_bytes": (SZ, []),
         "splitee_sensitivity": (I, [I, I64, P, P, D, D, P, P, SZ, P]),
         "splitee_eps_per_token": (I, [D, I64, P]),
+        "splitee_bank_path": (I, [ctypes.c_char_p, I64, I64, U64, ctypes.c_char_p, SZ]),
+        "splitee_bank_workspace_bytes": (SZ, [I64, I64, I]),
+        "splitee_bank_create": (I, [ctypes.c_char_p, P, I, I64, I64, I64, I, D, D, U64, U64, U64, I64, I, P, SZ,
+                                    P]),
+        "splitee_bank_open": (I, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p)]),
+        "splitee_bank_info": (I, [P, ctypes.POINTER(BankInfo)]),
+        "splitee_bank_load": (I, [P, I64, P, I64, I, ctypes.POINTER(ctypes.c_int64), P]),
+        "splitee_bank_close": (I, [P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -248,6 +271,53 @@ def splitee_eps_per_token(eps_total, n):
     return eps.value
 
 
+def splitee_bank_path(directory, K, N, stream_id):
+    buf = ctypes.create_string_buffer(4096)
+    _check("splitee_bank_path", load().splitee_bank_path(os.fsencode(directory), K, N, stream_id, buf, 4096))
+    return os.fsdecode(buf.value)
+
+
+def splitee_bank_workspace_bytes(K, N, prec):
+    return load().splitee_bank_workspace_bytes(K, N, prec)
+
+
+def splitee_bank_create(path, W, w_type, ldw, K, N, mech, sensitivity, epsilon, seed, stream_id, row0, rows, prec,
+                        workspace, workspace_bytes, stream=None):
+    _check("splitee_bank_create", load().splitee_bank_create(
+        os.fsencode(path), _ptr(W), w_type, ldw, K, N, mech, sensitivity, epsilon, seed, stream_id, row0, rows,
+        prec, _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def splitee_bank_open(path):
+    """Returns the bank handle (an integer address)."""
+    h = ctypes.c_void_p()
+    _check("splitee_bank_open", load().splitee_bank_open(os.fsencode(path), ctypes.byref(h)))
+    return h.value
+
+
+def splitee_bank_info(bank):
+    info = BankInfo()
+    _check("splitee_bank_info", load().splitee_bank_info(bank, ctypes.byref(info)))
+    return info.as_dict()
+
+
+def splitee_bank_load(bank, rows, C, ldc, dst_device, stream=None):
+    """C: a device tensor (dst_device true) or a host address / contiguous CPU tensor;
+    returns the first stream row of the loaded rows."""
+    row0 = ctypes.c_int64()
+    if dst_device:
+        ptr = _ptr(C)
+    else:
+        ptr = C if isinstance(C, int) or C is None else C.data_ptr()
+    _check("splitee_bank_load", load().splitee_bank_load(bank, rows, ptr, ldc, 1 if dst_device else 0,
+                                                         ctypes.byref(row0), _stream(stream) if dst_device else None))
+    return row0.value
+
+
+def splitee_bank_close(bank):
+    _check("splitee_bank_close", load().splitee_bank_close(bank))
+
+
 # ------------------------------------------------- tensor-level conveniences
 
 def _aligned_bytes(nbytes, device):
@@ -264,6 +334,16 @@ def spectral_norm(W, iters, seed, stream_id, history=False, ws=None):
         ws = _aligned_bytes(nbytes, W.device)
     return splitee_spectral_norm(W, _wtype(W), W.stride(0), N, K, iters, seed, stream_id, ws, nbytes,
                                  history=history)
+
+
+def bank_create(path, W, K, mech, sensitivity, epsilon, seed, stream_id, row0, rows, prec=SPLITEE_PREC_BF16X3):
+    """Precompute and store the corrections of W (N x K) for `rows` stream rows."""
+    N = W.shape[0]
+    nbytes = splitee_bank_workspace_bytes(K, N, prec)
+    ws = torch.zeros(nbytes + 256, dtype=torch.uint8, device=W.device)
+    ws = ws[(-ws.data_ptr()) % 256:][:nbytes]
+    splitee_bank_create(path, W, _wtype(W), W.stride(0), K, N, mech, sensitivity, epsilon, seed, stream_id, row0,
+                        rows, prec, ws, nbytes)
 
 
 def sensitivity(bound, alpha, beta=None, w_norm_a=0.0, w_norm_b=0.0):

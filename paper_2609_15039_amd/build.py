@@ -28,9 +28,10 @@ def _compile(src):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip and link libsplitee.so; returns its path."""
+    """Compile every csrc/*.hip and csrc/*.cpp and link libsplitee.so; returns its path."""
     os.makedirs(OBJ, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    # *.hip: device and host code; *.cpp: host-only code (the noise bank), same compiler
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     tmp = LIB + ".tmp%d" % os.getpid()

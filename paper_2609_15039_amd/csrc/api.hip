@@ -126,6 +126,10 @@ const char* splitee_status_string(int status)
     case SPLITEE_ERR_UNSUPPORTED: return "unsupported precision / data type combination";
     case SPLITEE_ERR_HIP: return "HIP launch failed";
     case SPLITEE_ERR_WORKSPACE: return "workspace missing or too small";
+    case SPLITEE_ERR_IO: return "bank file could not be created, opened, read or written";
+    case SPLITEE_ERR_EXHAUSTED: return "noise bank has fewer unused rows than requested";
+    case SPLITEE_ERR_FORMAT: return "bank file header or size is invalid";
+    case SPLITEE_ERR_BUSY: return "bank file is open in another handle";
     default: return "unknown status";
     }
 }
