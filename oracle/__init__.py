@@ -18,6 +18,7 @@ is the plain definition written out:
   unmask      Y        = fl32(R - C)                        -- ``unmask``
   reference   Y*       = X . W^T in binary64                -- ``gemm64``
   bounds      Theorem 4 and Eq. fp-log-bound per element    -- ``error_bounds``
+  binary64    Xt = fl64(X + eta) and its bound (Down)         -- ``mask64``, ``error_bounds_f64``
 
 Layouts: X is M x K (tokens x in-features), W is N x K (out x in, the paper's
 d' x d matrix acting on column vectors), Y = X W^T is M x N.
@@ -35,6 +36,7 @@ PREC_F32, PREC_BF16, PREC_BF16X3 = 0, 1, 2
 FN_LAPLACE_T, FN_GAUSS_R, FN_COS2PI, FN_SIN2PI = 0, 1, 2, 3
 
 U32 = 2.0 ** -24  # unit round-off of binary32 (Eq. ulp with p = 24)
+U64 = 2.0 ** -53  # unit round-off of binary64 (p = 53)
 U_BF16 = 2.0 ** -8  # unit round-off of bfloat16 (p = 8)
 
 _lib = None
@@ -247,6 +249,35 @@ def error_bounds(X, eta, Xt, W, prec=PREC_F32, k_acc=None):
     precond = Se <= (K - 1) * Sx
     return dict(Sx=Sx, St=St, Se=Se, thm4=thm4, logb=logb, rigor=rigor, gate=gate,
                 precond=precond)
+
+
+def mask64(X, eta):
+    """Xt = fl64(X + eta): the mask in binary64, one addition of the binary32 operands
+    (the remedy the paper names for the Down projection, Sec. "The Case Against the
+    Down Linear Projection": binary64 instead of binary32)."""
+    return np.asarray(X, dtype=np.float32).astype(np.float64) + np.asarray(eta, dtype=np.float32).astype(np.float64)
+
+
+def error_bounds_f64(X, eta, W):
+    """Per-element bound for Y = fl32(fl64(fl64(Xt W^T) - fl64(eta W^T))) against X W^T,
+    Xt = fl64(X + eta): the derivation of Theorem 4 with the unit roundoff of binary64
+    for the mask and both products, then one binary64 subtraction and one rounding to
+    binary32.  With u = 2^-53, S_x, S_t (|Xt|) and S_e as in error_bounds:
+
+      E     = gamma_K(u) (S_t + S_e) + 2 u S_t      products (any order) and the mask
+      bound = E + (u32 + 2 u)(S_x + E)              subtraction, rounding to binary32
+      thm4  = gamma_K(u) (S_x + S_t + S_e) + u S_x  Theorem 4 itself at u = 2^-53
+    """
+    Wa = np.abs(np.asarray(W, dtype=np.float64))
+    K = Wa.shape[1]
+    Sx = np.abs(np.asarray(X, dtype=np.float64)) @ Wa.T
+    St = np.abs(mask64(X, eta)) @ Wa.T
+    Se = np.abs(np.asarray(eta, dtype=np.float64)) @ Wa.T
+    g = gamma(K, U64)
+    E = g * (St + Se) + 2.0 * U64 * St
+    bound = E + (U32 + 2.0 * U64) * (Sx + E)
+    thm4 = g * (Sx + St + Se) + U64 * Sx
+    return dict(Sx=Sx, St=St, Se=Se, E=E, bound=bound, thm4=thm4)
 
 
 def dot_bound(A, W, k_acc=None):

@@ -183,3 +183,83 @@ def test_gamma_definition_domain():
         O.gamma(2**24)
     # Eq. fp-log-bound uses gamma_{ceil(log2 d)+1}: d = 3072 -> gamma_13
     assert math.ceil(math.log2(3072)) + 1 == 13
+
+
+# ------------------------------------------------------------------ binary64 path
+
+DELTA_ACT = 1.66e8  # Theorem 3 for a Llama-3.2-3B-shaped layer with random weights
+
+
+def _fp64_path(X, eta, W, seq=False):
+    Xt = O.mask64(X, eta)
+    W64 = np.asarray(W, dtype=np.float64)
+    e64 = np.asarray(eta, dtype=np.float64)
+    if not seq:
+        R, C = Xt @ W64.T, e64 @ W64.T
+    else:
+        def seqdot(A):
+            acc = np.zeros((A.shape[0], W64.shape[0]))
+            for k in range(A.shape[1]):
+                acc = acc + A[:, k:k + 1] * W64[:, k][None, :]
+            return acc
+        R, C = seqdot(Xt), seqdot(e64)
+    return (R - C).astype(np.float32)
+
+
+def test_mask64_is_one_binary64_addition():
+    g = np.random.Generator(np.random.PCG64(4))
+    x = g.standard_normal(4096).astype(np.float32)
+    e = (g.standard_normal(4096) * DELTA_ACT).astype(np.float32)
+    got = O.mask64(x, e)
+    want = np.array([float(Fraction(float(a)) + Fraction(float(b))) for a, b in zip(x[:64], e[:64])])
+    assert np.array_equal(got[:64], want)  # correctly rounded sum
+    # where |eta| < 2^28 |x| the sum is exact, so x comes back unchanged
+    back = (got - e.astype(np.float64)).astype(np.float32)
+    exact = np.abs(e) < np.abs(x) * 2.0 ** 28
+    assert exact.mean() > 0.5 and np.array_equal(back[exact], x[exact])
+
+
+@pytest.mark.parametrize("delta,eps", [(1.0, 1.0), (825.27, 0.5), (DELTA_ACT, 1.0), (DELTA_ACT, 0.25)])
+@pytest.mark.parametrize("seq", [False, True])
+def test_f64_bound_covers_real_binary64_execution(delta, eps, seq):
+    M, K, N = 4, 1024 if seq else 8192, 24
+    X = WL.gen_x(M, K, seed=1)
+    W = WL.gen_w(N, K, seed=2)
+    eta = O.noise(M, K, O.MECH_GAUSSIAN, delta, eps, 0, 3)
+    Y = _fp64_path(X, eta, W, seq)
+    err = np.abs(Y.astype(np.float64) - O.gemm64(X, W))
+    b = O.error_bounds_f64(X, eta, W)
+    assert np.all(err <= b["bound"])
+    # Theorem 4 at u = 2^-53 is gamma_K(u64) / gamma_K(u32) ~ 2^-29 of the binary32 bound
+    b32 = O.error_bounds(X, eta, O.mask(X, eta), W)
+    assert np.allclose(b["thm4"] / b32["thm4"], 2.0 ** -29, rtol=1e-3)
+
+
+def test_f64_bound_noise_terms_are_load_bearing():
+    # at the sensitivity of Theorem 3 the binary64 product roundings show: the error is
+    # more than the final rounding of the exact result to binary32 could explain
+    M, K, N = 4, 8192, 32
+    X = WL.gen_x(M, K, seed=1)
+    W = WL.gen_w(N, K, seed=2)
+    eta = O.noise(M, K, O.MECH_GAUSSIAN, DELTA_ACT, 1.0, 0, 3)
+    y = O.gemm64(X, W)
+    err = np.abs(_fp64_path(X, eta, W, seq=True).astype(np.float64) - y)
+    b = O.error_bounds_f64(X, eta, W)
+    assert np.any(err > 4 * O.U32 * np.abs(y))
+    assert np.all(err <= b["bound"])
+
+
+def test_binary64_remedies_the_down_projection():
+    # the paper's case against offloading Down in binary32: at Theorem 3's sensitivity the
+    # binary32 masked product loses X entirely, the binary64 one keeps it
+    M, K, N = 4, 8192, 32
+    X = WL.gen_x(M, K, seed=1)
+    W = WL.gen_w(N, K, seed=2)
+    eta = O.noise(M, K, O.MECH_GAUSSIAN, DELTA_ACT, 1.0, 0, 3)
+    y = O.gemm64(X, W)
+    _, Y32 = _fp32_path(X, eta, W)
+    Y64 = _fp64_path(X, eta, W)
+    rel32 = np.median(np.abs(Y32 - y) / np.abs(y))
+    rel64 = np.median(np.abs(Y64 - y) / np.abs(y))
+    assert rel32 > 0.5  # fl32(x + eta) drops x: the binary32 result is about 0, error ~ |y|
+    assert rel64 < 1e-3
