@@ -23,7 +23,9 @@ they run on; ``traffic`` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
 summary of the workload when the kernel sources still match it, else null),
 ``cpu_baseline`` (the CPU oracle on a bounded sample of the same workload),
 ``modes`` (other precision modes), ``correction_ms`` (offline precompute),
-``noise_bank`` (one layer's correction banks for 2048 positions: created from the
+``down_f64`` (the Down projection at Theorem 3's noise scale through the binary64
+path against the bf16x3 one: time and error), ``noise_bank`` (one layer's correction
+banks for 2048 positions: created from the
 GPU corrections into files, then loaded as decode steps and as one batch),
 ``noise_scale`` (the offline noise-scale step of the same model: spectral norms
 of W_val, W_up and W_gate by the power method, the sensitivity bounds of
@@ -63,6 +65,8 @@ def parse():
     ap.add_argument("--noise-scale-only", action="store_true", help="run only the noise-scale leg")
     ap.add_argument("--power-iters", type=int, default=300)
     ap.add_argument("--no-noise-bank", action="store_true", help="skip the noise-bank leg")
+    ap.add_argument("--no-down-f64", action="store_true", help="skip the binary64 Down leg")
+    ap.add_argument("--down-f64-only", action="store_true", help="run only the binary64 Down leg")
     ap.add_argument("--noise-bank-only", action="store_true", help="run only the noise-bank leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (HBM counter calibration) and exit")
@@ -495,6 +499,61 @@ def noise_bank_leg(torch, sp, WL, workload, rows=2048):
             "batch_load_GBps": round(rest * row_bytes / t_batch / 1e9, 3)}
 
 
+F64_PEAK_TFS = 78.6
+
+
+def down_f64_leg(torch, sp, WL, workload, M=128, delta=1.66e8, eps=1.0, reps=20):
+    """The Down projection of the workload's model at 128 tokens with the noise scale of
+    Theorem 3 (Delta about 1.66e8 for random-init Llama-shaped weights, eps = 1): the
+    binary64 fused call against the binary32-accurate (bf16x3) one, time per call (HIP
+    events on the stream the kernels run on, mean of `reps` calls) and the error of each
+    against X W^T evaluated in binary64 on the GPU (a reference for this figure only)."""
+    model = WL.QWEN3_4B if workload.startswith("qwen") else WL.LLAMA_3B
+    K, N = model.ff, model.hidden
+    g = torch.Generator(device="cuda")
+    g.manual_seed(13)
+    X = torch.randn((M, K), generator=g, device="cuda")
+    W = (torch.randn((N, K), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    G = sp.SPLITEE_MECH_GAUSSIAN
+    sid = WL.stream_id(0, 3)
+    C64 = sp.correction_f64(W, M, G, delta, eps, 0, sid, 0)
+    C32 = sp.correction(W, M, G, delta, eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
+    ws64 = sp.workspace_f64(M, N, K)
+    ws32 = sp.workspace(M, N, K, sp.SPLITEE_PREC_BF16X3)
+    Y64 = torch.empty((M, N), device="cuda")
+    Y32 = torch.empty((M, N), device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        b.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    t64 = timed(lambda: sp.masked_linear_fused_f64(X, W, C64, G, delta, eps, 0, sid, 0, ws=ws64, Y=Y64))
+    t32 = timed(lambda: sp.masked_linear_fused(X, W, C32, G, delta, eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3,
+                                               ws=ws32, Y=Y32))
+    ref = X.double() @ W.double().t()
+    den = ref.abs()
+    rel64 = ((Y64.double() - ref).abs() / den)
+    rel32 = ((Y32.double() - ref).abs() / den)
+    flops = 2.0 * M * N * K
+    tf = flops / (t64 * 1e-6) / 1e12
+    return {"model": model.name, "projection": "down", "tokens": M, "K": K, "N": N, "delta": delta, "eps": eps,
+            "f64_us": round(t64, 1), "bf16x3_us": round(t32, 1), "cost_ratio": round(t64 / t32, 2),
+            "f64_rel_error_median": float("%.3g" % rel64.median().item()),
+            "f64_rel_error_max": float("%.3g" % rel64.max().item()),
+            "bf16x3_rel_error_median": float("%.3g" % rel32.median().item()),
+            "roofline": {"bound": "mfma", "kernel": "mask (binary64) + gemm_f64_kernel + f64_sum_kernel",
+                         "achieved": round(tf, 2), "peak": F64_PEAK_TFS, "unit": "TFLOP/s",
+                         "frac": round(tf / F64_PEAK_TFS, 4)}}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -518,6 +577,9 @@ def main():
         prec = sp.SPLITEE_PREC_F32
     if args.counter_launches:
         counter_launches(torch, sp, WL, args, prec)
+        return
+    if args.down_f64_only:
+        print(json.dumps({"down_f64": down_f64_leg(torch, sp, WL, args.workload)}), flush=True)
         return
     if args.noise_bank_only:
         print(json.dumps({"noise_bank": noise_bank_leg(torch, sp, WL, args.workload)}), flush=True)
@@ -584,6 +646,8 @@ def main():
         "correction_ms": round(path.correction_ms, 4),
         "modes": modes,
     }
+    if not args.no_down_f64:
+        out["down_f64"] = down_f64_leg(torch, sp, WL, args.workload)
     if not args.no_noise_bank:
         out["noise_bank"] = noise_bank_leg(torch, sp, WL, args.workload)
     if not args.no_noise_scale:

@@ -96,7 +96,12 @@ typedef enum {
 
 typedef enum { SPLITEE_MECH_LAPLACE = 0, SPLITEE_MECH_GAUSSIAN = 1, SPLITEE_MECH_NONE = 2 } splitee_mech;
 typedef enum { SPLITEE_F32 = 0, SPLITEE_BF16 = 1 } splitee_dtype;
-typedef enum { SPLITEE_PREC_F32 = 0, SPLITEE_PREC_BF16 = 1, SPLITEE_PREC_BF16X3 = 2 } splitee_prec;
+typedef enum {
+    SPLITEE_PREC_F32 = 0,
+    SPLITEE_PREC_BF16 = 1,
+    SPLITEE_PREC_BF16X3 = 2,
+    SPLITEE_PREC_F64 = 3 /* binary64 mask, GEMM and correction: only the *_f64 entry points */
+} splitee_prec;
 
 /* Version of this ABI (SPLITEE_ABI_VERSION). */
 int splitee_abi_version(void);
@@ -143,9 +148,11 @@ int splitee_noise_gen_multi(float* const* eta, const int64_t* ld_eta, const int6
  * Mask: Xt = fl32(X + eta) (the vector addition of Sec. "Offloading Linear
  * Operations"), written in precision out_prec:
  *   F32: float32 M x K (ldxt); BF16: one bfloat16 plane; BF16X3: three bfloat16
- *   planes hi, mid, lo (plane p at Xt + p * M * ldxt).
+ *   planes hi, mid, lo (plane p at Xt + p * M * ldxt); F64: binary64 M x K holding
+ *   fl64(X + eta) instead (the operand of the *_f64 entry points).
  *   X may be NULL, meaning X = 0 (used to split eta for the correction).
- * Requires K % 4 == 0; ldxt a multiple of 8 for bfloat16 output, of 4 for float32.
+ * Requires K % 4 == 0; ldxt a multiple of 8 for bfloat16 output, of 4 for float32,
+ * of 2 for binary64.
  */
 int splitee_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, void* Xt,
                  int out_prec, int64_t ldxt, int64_t M, int64_t K, void* stream);
@@ -244,6 +251,35 @@ int splitee_correction(float* C, int64_t ldc, const void* W, int w_type, int64_t
  */
 int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_slow, float* out,
                             void* stream);
+
+/*
+ * Binary64 variant of the fused call and the correction (SPLITEE_PREC_F64): for a
+ * projection whose noise scale is too large for binary32 cancellation, as for the Down
+ * projection under Theorem 3 (Sec. "The Case Against the Down Linear Projection": with
+ * the unit roundoff of binary64 the error bound of Theorem 4 shrinks by about 2^29).
+ *   Xt = fl64(X + eta) with eta the binary32 noise of splitee_noise_gen (the sum is exact
+ *   while |X| and |eta| are within a factor 2^29); R = Xt W^T accumulated in binary64
+ *   (W bfloat16 or float32, exact in binary64); Y = fl32(R - C).
+ *   C          M x N binary64 correction from splitee_correction_f64 with the same noise
+ *              arguments, leading dimension ldc >= N, 16-byte aligned
+ *   X, Y       as in splitee_masked_linear_fused (float32)
+ *   workspace  >= splitee_f64_workspace_bytes(M, N, K) bytes, 256-byte aligned, no
+ *              initial contents needed (the binary64 Xt and, for small tile counts, the
+ *              split-K partials)
+ * Requires K % 8 == 0.
+ */
+size_t splitee_f64_workspace_bytes(int64_t M, int64_t N, int64_t K);
+int splitee_masked_linear_fused_f64(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
+                                    const double* C, int64_t ldc, float* Y, int64_t ldy, int64_t M, int64_t N,
+                                    int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                                    uint64_t stream_id, uint64_t row0, void* workspace, size_t workspace_bytes,
+                                    void* stream);
+
+/* C = eta W^T in binary64 (M x N, leading dimension ldc >= N, 16-byte aligned); noise
+ * and W arguments as for splitee_masked_linear_fused_f64. */
+int splitee_correction_f64(double* C, int64_t ldc, const void* W, int w_type, int64_t ldw, int64_t M, int64_t N,
+                           int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                           uint64_t stream_id, uint64_t row0, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Noise scale (Prop. 2: the Gaussian mask has standard deviation Delta f / eps per

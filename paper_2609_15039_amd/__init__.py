@@ -31,7 +31,9 @@ EXPORTED = [
     "splitee_sensitivity_workspace_bytes", "splitee_sensitivity", "splitee_eps_per_token",
     "splitee_bank_path", "splitee_bank_workspace_bytes", "splitee_bank_create", "splitee_bank_open",
     "splitee_bank_info", "splitee_bank_load", "splitee_bank_close",
+    "splitee_f64_workspace_bytes", "splitee_masked_linear_fused_f64", "splitee_correction_f64",
 ]
+SPLITEE_PREC_F64 = 3
 SPLITEE_ERR_IO, SPLITEE_ERR_EXHAUSTED, SPLITEE_ERR_FORMAT, SPLITEE_ERR_BUSY = -8, -9, -10, -11
 
 
@@ -97,6 +99,10 @@ def load():
         "splitee_bank_info": (I, [P, ctypes.POINTER(BankInfo)]),
         "splitee_bank_load": (I, [P, I64, P, I64, I, ctypes.POINTER(ctypes.c_int64), P]),
         "splitee_bank_close": (I, [P]),
+        "splitee_f64_workspace_bytes": (SZ, [I64, I64, I64]),
+        "splitee_masked_linear_fused_f64": (I, [P, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, I, D, D, U64,
+                                                U64, U64, P, SZ, P]),
+        "splitee_correction_f64": (I, [P, I64, P, I, I64, I64, I64, I64, I, D, D, U64, U64, U64, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -271,6 +277,24 @@ def splitee_eps_per_token(eps_total, n):
     return eps.value
 
 
+def splitee_f64_workspace_bytes(M, N, K):
+    return load().splitee_f64_workspace_bytes(M, N, K)
+
+
+def splitee_masked_linear_fused_f64(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, mech, sensitivity, epsilon,
+                                    seed, stream_id, row0, workspace, workspace_bytes, stream=None):
+    _check("splitee_masked_linear_fused_f64", load().splitee_masked_linear_fused_f64(
+        _ptr(X), ldx, _ptr(W), w_type, ldw, _ptr(C), ldc, _ptr(Y), ldy, M, N, K, mech, sensitivity, epsilon, seed,
+        stream_id, row0, _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def splitee_correction_f64(C, ldc, W, w_type, ldw, M, N, K, mech, sensitivity, epsilon, seed, stream_id, row0,
+                           workspace, workspace_bytes, stream=None):
+    _check("splitee_correction_f64", load().splitee_correction_f64(
+        _ptr(C), ldc, _ptr(W), w_type, ldw, M, N, K, mech, sensitivity, epsilon, seed, stream_id, row0,
+        _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
 def splitee_bank_path(directory, K, N, stream_id):
     buf = ctypes.create_string_buffer(4096)
     _check("splitee_bank_path", load().splitee_bank_path(os.fsencode(directory), K, N, stream_id, buf, 4096))
@@ -336,6 +360,34 @@ def spectral_norm(W, iters, seed, stream_id, history=False, ws=None):
                                  history=history)
 
 
+def workspace_f64(M, N, K, device="cuda"):
+    """A 256-byte aligned workspace for the binary64 calls; returns (tensor, bytes)."""
+    nbytes = splitee_f64_workspace_bytes(M, N, K)
+    return _aligned_bytes(nbytes, device), nbytes
+
+
+def correction_f64(W, M, mech, sensitivity, epsilon, seed, stream_id, row0=0, ws=None):
+    N, K = W.shape
+    C = torch.empty((M, N), dtype=torch.float64, device=W.device)
+    if ws is None:
+        ws = workspace_f64(M, N, K, W.device)
+    splitee_correction_f64(C, N, W, _wtype(W), W.stride(0), M, N, K, mech, sensitivity, epsilon, seed, stream_id,
+                           row0, ws[0], ws[1])
+    return C
+
+
+def masked_linear_fused_f64(X, W, C, mech, sensitivity, epsilon, seed, stream_id, row0=0, ws=None, Y=None):
+    M, K = X.shape
+    N = W.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = workspace_f64(M, N, K, X.device)
+    splitee_masked_linear_fused_f64(X, X.stride(0), W, _wtype(W), W.stride(0), C, C.stride(0), Y, Y.stride(0), M,
+                                    N, K, mech, sensitivity, epsilon, seed, stream_id, row0, ws[0], ws[1])
+    return Y
+
+
 def bank_create(path, W, K, mech, sensitivity, epsilon, seed, stream_id, row0, rows, prec=SPLITEE_PREC_BF16X3):
     """Precompute and store the corrections of W (N x K) for `rows` stream rows."""
     N = W.shape[0]
@@ -388,7 +440,7 @@ def masked_linear(Xt, prec, W):
 def noise_mask(X, prec, mech, sensitivity, epsilon, seed, stream_id, row0=0):
     M, K = X.shape
     planes = 3 if prec == SPLITEE_PREC_BF16X3 else 1
-    dt = torch.float32 if prec == SPLITEE_PREC_F32 else torch.int16
+    dt = {SPLITEE_PREC_F32: torch.float32, SPLITEE_PREC_F64: torch.float64}.get(prec, torch.int16)
     Xt = torch.empty((planes, M, K), dtype=dt, device=X.device)
     splitee_noise_mask(X, X.stride(0), Xt, prec, K, M, K, mech, sensitivity, epsilon, seed,
                        stream_id, row0)

@@ -37,7 +37,7 @@ inline bool dims_ok(int64_t M, int64_t N, int64_t K)
     return M >= 0 && N >= 0 && K >= 0 && M <= MAX_DIM && N <= MAX_DIM && K <= MAX_DIM;
 }
 
-inline int64_t prec_elsize(int prec) { return prec == SPLITEE_PREC_F32 ? 4 : 2; }
+inline int64_t prec_elsize(int prec) { return prec == SPLITEE_PREC_F64 ? 8 : prec == SPLITEE_PREC_F32 ? 4 : 2; }
 inline int64_t prec_planes(int prec) { return prec == SPLITEE_PREC_BF16X3 ? 3 : 1; }
 inline bool valid_prec(int prec)
 {
@@ -109,6 +109,39 @@ int run_masked(const float* X, int64_t ldx, const void* W, int w_type, int64_t l
     return run_gemm(Xt, prec, K, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, base, gws, s);
 }
 
+// Binary64 path: the mask fl64(X + eta) (or eta alone for the correction) into the
+// workspace, then the binary64 GEMM with the unmask epilogue.
+size_t f64_ws(int64_t M, int64_t N, int64_t K)
+{
+    return align256((size_t)M * K * 8) + align256(splitee_host::f64_gemm_workspace_bytes(M, N, K));
+}
+
+int run_f64(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw, const double* C, int64_t ldc,
+            void* Out, bool out64, int64_t ldo, int64_t M, int64_t N, int64_t K, int mech, double sensitivity,
+            double epsilon, uint64_t seed, uint64_t sid, uint64_t row0, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    const size_t need = f64_ws(M, N, K);
+    if (ws_bytes < need || (need > 0 && ws == nullptr)) return SPLITEE_ERR_WORKSPACE;
+    if (ws && (reinterpret_cast<uintptr_t>(ws) & 255u)) return SPLITEE_ERR_ALIGN;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    char* base = reinterpret_cast<char*>(ws);
+    double* Xt = reinterpret_cast<double*>(base);
+    const size_t xt_bytes = align256((size_t)M * K * 8);
+    int rc = splitee_host::launch_mask(X, ldx, nullptr, 0, mech, sensitivity / epsilon, seed, sid, row0, Xt,
+                                       SPLITEE_PREC_F64, K, 0, M, K, nullptr, 0, s);
+    if (rc != SPLITEE_OK) return rc;
+    return splitee_host::launch_gemm_f64(Xt, K, W, w_type, ldw, C, ldc, Out, out64, ldo, M, N, K, base + xt_bytes,
+                                         ws_bytes - xt_bytes, s);
+}
+
+int check_w_f64(const void* W, int w_type, int64_t ldw, int64_t K)
+{
+    if (!valid_dtype(w_type)) return SPLITEE_ERR_DTYPE;
+    if (ldw < K) return SPLITEE_ERR_SHAPE;
+    if (!aligned16(W) || !pitch16(ldw, w_type == SPLITEE_F32 ? 4 : 2)) return SPLITEE_ERR_ALIGN;
+    return SPLITEE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -175,7 +208,7 @@ int splitee_noise_gen_multi(float* const* eta, const int64_t* ld_eta, const int6
 int splitee_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, void* Xt,
                  int out_prec, int64_t ldxt, int64_t M, int64_t K, void* stream)
 {
-    if (!valid_prec(out_prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!valid_prec(out_prec) && out_prec != SPLITEE_PREC_F64) return SPLITEE_ERR_UNSUPPORTED;
     if (!dims_ok(M, 0, K) || K % 4 != 0 || ld_eta < K || ldxt < K || (X && ldx < K))
         return SPLITEE_ERR_SHAPE;
     if (M == 0 || K == 0) return SPLITEE_OK;
@@ -195,7 +228,7 @@ int splitee_noise_mask(const float* X, int64_t ldx, void* Xt, int out_prec, int6
 {
     int rc = check_noise_args(mech, sensitivity, epsilon);
     if (rc) return rc;
-    if (!valid_prec(out_prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!valid_prec(out_prec) && out_prec != SPLITEE_PREC_F64) return SPLITEE_ERR_UNSUPPORTED;
     if (!dims_ok(M, 0, K) || K % 4 != 0 || ldxt < K || (X && ldx < K)) return SPLITEE_ERR_SHAPE;
     if (M == 0 || K == 0) return SPLITEE_OK;
     if (!Xt) return SPLITEE_ERR_ARG;
@@ -319,6 +352,46 @@ int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_
     if (n == 0) return SPLITEE_OK;
     if (!words || !out) return SPLITEE_ERR_ARG;
     return splitee_host::launch_transform_probe(words, n, fn, force_slow, out, as_stream(stream));
+}
+
+size_t splitee_f64_workspace_bytes(int64_t M, int64_t N, int64_t K)
+{
+    if (!dims_ok(M, N, K) || K % 8 != 0) return 0;
+    return f64_ws(M, N, K);
+}
+
+int splitee_masked_linear_fused_f64(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
+                                    const double* C, int64_t ldc, float* Y, int64_t ldy, int64_t M, int64_t N,
+                                    int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                                    uint64_t stream_id, uint64_t row0, void* workspace, size_t workspace_bytes,
+                                    void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldx < K || ldc < N || ldy < N) return SPLITEE_ERR_SHAPE;
+    rc = check_w_f64(W, w_type, ldw, K);
+    if (rc) return rc;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!X || !W || !C || !Y) return SPLITEE_ERR_ARG;
+    if (!aligned16(X) || !pitch16(ldx, 4) || !aligned16(C) || !aligned16(Y)) return SPLITEE_ERR_ALIGN;
+    return run_f64(X, ldx, W, w_type, ldw, C, ldc, Y, false, ldy, M, N, K, mech, sensitivity, epsilon, seed,
+                   stream_id, row0, workspace, workspace_bytes, as_stream(stream));
+}
+
+int splitee_correction_f64(double* C, int64_t ldc, const void* W, int w_type, int64_t ldw, int64_t M, int64_t N,
+                           int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                           uint64_t stream_id, uint64_t row0, void* workspace, size_t workspace_bytes, void* stream)
+{
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldc < N) return SPLITEE_ERR_SHAPE;
+    rc = check_w_f64(W, w_type, ldw, K);
+    if (rc) return rc;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!W || !C) return SPLITEE_ERR_ARG;
+    if (!aligned16(C)) return SPLITEE_ERR_ALIGN;
+    return run_f64(nullptr, K, W, w_type, ldw, nullptr, 0, C, true, ldc, M, N, K, mech, sensitivity, epsilon,
+                   seed, stream_id, row0, workspace, workspace_bytes, as_stream(stream));
 }
 
 size_t splitee_spectral_norm_workspace_bytes(int64_t N, int64_t K, int iters)

@@ -77,6 +77,11 @@ size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
 int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
                   int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,
                   int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+// Binary64 GEMM Out = A W^T (- C), A binary64, W bf16 / f32, Out binary64 or rounded to binary32.
+size_t f64_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+int launch_gemm_f64(const double* A, int64_t lda, const void* W, int w_type, int64_t ldw, const double* C,
+                    int64_t ldc, void* Out, bool out64, int64_t ldo, int64_t M, int64_t N, int64_t K, void* ws,
+                    size_t ws_bytes, hipStream_t s);
 // Power method for ||W||_2 and the vector norms of the sensitivity bounds.
 size_t spectral_workspace_bytes(int64_t N, int64_t K, int iters);
 int spectral_max_k();

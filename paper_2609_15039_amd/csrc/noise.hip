@@ -87,6 +87,16 @@ __global__ void __launch_bounds__(256) mask_kernel(
         } else {
             e = *reinterpret_cast<const float2*>(eta + i * ld_eta + 2 * c);
         }
+        if (PREC == SPLITEE_PREC_F64) {
+            // one binary64 addition: exact whenever x and eta are within 2^29 of each other in magnitude
+            double2 xd = make_double2((double)e.x, (double)e.y);
+            if (X) {
+                const float2 x = *reinterpret_cast<const float2*>(X + i * ldx + 2 * c);
+                xd = make_double2((double)x.x + xd.x, (double)x.y + xd.y);
+            }
+            *reinterpret_cast<double2*>(reinterpret_cast<double*>(Xt) + i * ldxt + 2 * c) = xd;
+            continue;
+        }
         float2 xt;
         if (X) {
             const float2 x = *reinterpret_cast<const float2*>(X + i * ldx + 2 * c);
@@ -188,8 +198,10 @@ int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, i
         if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F32, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F32, false);
     } else if (prec == SPLITEE_PREC_BF16) {
         if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16, false);
-    } else {
+    } else if (prec == SPLITEE_PREC_BF16X3) {
         if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16X3, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16X3, false);
+    } else {
+        if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F64, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F64, false);
     }
 #undef SPLITEE_MASK_LAUNCH
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;

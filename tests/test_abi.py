@@ -220,3 +220,30 @@ def test_eps_per_token_validation(lib, eps, n):
     out = ctypes.c_double()
     assert lib.splitee_eps_per_token(eps, n, ctypes.byref(out)) == ARG
     assert lib.splitee_eps_per_token(1.0, 4, None) == ARG
+
+
+def f64_fused(lib, X=P, ldx=8, W=P, wt=BF16, ldw=8, C=P, ldc=8, Y=P, ldy=8, M=2, N=8, K=8, mech=G, d=1.0, e=1.0,
+              ws=256, wsb=1 << 20):
+    return lib.splitee_masked_linear_fused_f64(X, ldx, W, wt, ldw, C, ldc, Y, ldy, M, N, K, mech, d, e, 0, 0, 0, ws,
+                                               wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(e=0.0), ARG), (dict(mech=3), ARG), (dict(K=12, ldx=12, ldw=16), SHAPE), (dict(ldc=4), SHAPE),
+    (dict(ldy=4), SHAPE), (dict(ldx=4), SHAPE), (dict(wt=7), DTYPE), (dict(ldw=4), SHAPE), (dict(W=8), ALIGN),
+    (dict(X=None), ARG), (dict(C=None), ARG), (dict(Y=None), ARG), (dict(C=8), ALIGN), (dict(X=8), ALIGN),
+    (dict(ws=None, wsb=0), WS), (dict(wsb=64), WS), (dict(ws=16), ALIGN), (dict(M=0), OK), (dict(N=0), OK)])
+def test_fused_f64_validation(lib, kw, code):
+    assert f64_fused(lib, **kw) == code
+
+
+def test_correction_f64_validation_and_workspace(lib):
+    f = lib.splitee_correction_f64
+    assert f(P, 4, P, BF16, 8, 2, 8, 8, G, 1.0, 1.0, 0, 0, 0, 256, 1 << 20, None) == SHAPE
+    assert f(None, 8, P, BF16, 8, 2, 8, 8, G, 1.0, 1.0, 0, 0, 0, 256, 1 << 20, None) == ARG
+    assert f(P, 8, P, BF16, 8, 2, 8, 8, G, -1.0, 1.0, 0, 0, 0, 256, 1 << 20, None) == ARG
+    assert f(P, 8, P, BF16, 8, 2, 8, 8, G, 1.0, 1.0, 0, 0, 0, None, 0, None) == WS
+    q = lib.splitee_f64_workspace_bytes
+    assert q(2, 8, 6) == 0
+    assert q(128, 3072, 8192) >= 128 * 8192 * 8  # the binary64 masked input
+    assert q(128, 3072, 8192) % 256 == 0

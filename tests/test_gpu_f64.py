@@ -1,0 +1,104 @@
+"""GPU parity of the binary64 masked projection (the *_f64 entry points) against the
+oracle: the binary64 mask bit for bit, the binary64 correction within Higham's bound
+at u = 2^-53, the fused call within error_bounds_f64 (Theorem 4's derivation in
+binary64 plus the rounding to binary32) at the sensitivity of Theorem 3, and the
+contrast the paper draws: at that sensitivity the binary32-accurate path loses X."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2609_15039_amd as sp
+import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+G = sp.SPLITEE_MECH_GAUSSIAN
+DELTA_ACT = 1.66e8
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def dev_w(W, w_dtype):
+    t = dev(W)
+    return t.to(torch.bfloat16) if w_dtype == "bf16" else t
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+@pytest.mark.parametrize("with_x", [True, False])
+@pytest.mark.parametrize("delta", [1.0, DELTA_ACT])
+def test_mask64_bit_exact(with_x, delta):
+    M, K, sid = 37, 264, WL.stream_id(2, 3)
+    X = WL.gen_x(M, K, seed=4)
+    Xt = torch.full((M, K + 2), float("nan"), dtype=torch.float64, device=DEV)
+    sp.splitee_noise_mask(dev(X) if with_x else None, K, Xt, sp.SPLITEE_PREC_F64, K + 2, M, K, G, delta, 1.0, 5,
+                          sid, 17)
+    eta = O.noise(M, K, O.MECH_GAUSSIAN, delta, 1.0, 5, sid, 17)
+    want = O.mask64(X if with_x else np.zeros_like(X), eta)
+    got = host(Xt)
+    assert np.array_equal(got[:, :K].view(np.uint64), want.view(np.uint64))
+    assert np.all(np.isnan(got[:, K:]))
+
+
+SHAPES = [(37, 200, 264, "bf16"), (5, 64, 8, "f32"), (128, 3072, 8192, "bf16"), (64, 1000, 2560, "f32"),
+          (1, 6144, 2560, "bf16")]
+
+
+@pytest.mark.parametrize("M,N,K,wd", SHAPES)
+def test_correction_f64_within_binary64_bound(M, N, K, wd):
+    sid = WL.stream_id(7, 3)
+    W = WL.gen_w(N, K, seed=9, dtype=wd)
+    C = host(sp.correction_f64(dev_w(W, wd), M, G, DELTA_ACT, 1.0, 0, sid, 40))
+    eta = O.noise(M, K, O.MECH_GAUSSIAN, DELTA_ACT, 1.0, 0, sid, 40)
+    err = np.abs(C - O.gemm64(eta, W))
+    assert np.all(err <= O.gamma(K, O.U64) * (np.abs(eta).astype(np.float64) @ np.abs(W.astype(np.float64)).T))
+
+
+@pytest.mark.parametrize("M,N,K,wd", SHAPES)
+@pytest.mark.parametrize("delta,eps", [(1.0, 1.0), (825.27, 0.5), (DELTA_ACT, 1.0)])
+def test_fused_f64_within_bound(M, N, K, wd, delta, eps):
+    sid = WL.stream_id(7, 3)
+    X = WL.gen_x(M, K, seed=3)
+    W = WL.gen_w(N, K, seed=9, dtype=wd)
+    Wd = dev_w(W, wd)
+    C = sp.correction_f64(Wd, M, G, delta, eps, 0, sid, 0)
+    Y = host(sp.masked_linear_fused_f64(dev(X), Wd, C, G, delta, eps, 0, sid, 0))
+    eta = O.noise(M, K, O.MECH_GAUSSIAN, delta, eps, 0, sid, 0)
+    b = O.error_bounds_f64(X, eta, W)
+    err = np.abs(Y.astype(np.float64) - O.gemm64(X, W))
+    assert np.all(err <= b["bound"])
+
+
+def test_down_projection_at_theorem3_sensitivity():
+    # Llama-3.2-3B Down (8192 -> 3072), 128 tokens, Delta of Theorem 3: the binary32-accurate
+    # path returns about 0 (x is rounded away when masked), the binary64 path keeps X W^T
+    M, N, K = 128, 3072, 8192
+    sid = WL.stream_id(0, 3)
+    X = WL.gen_x(M, K, seed=3)
+    W = WL.gen_w(N, K, seed=10)
+    Wd = dev_w(W, "bf16")
+    y = O.gemm64(X, W)
+    C64 = sp.correction_f64(Wd, M, G, DELTA_ACT, 1.0, 0, sid, 0)
+    Y64 = host(sp.masked_linear_fused_f64(dev(X), Wd, C64, G, DELTA_ACT, 1.0, 0, sid, 0))
+    C32 = sp.correction(Wd, M, G, DELTA_ACT, 1.0, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
+    Y32 = host(sp.masked_linear_fused(dev(X), Wd, C32, G, DELTA_ACT, 1.0, 0, sid, 0, sp.SPLITEE_PREC_BF16X3))
+    rel64 = np.median(np.abs(Y64 - y) / np.abs(y))
+    rel32 = np.median(np.abs(Y32 - y) / np.abs(y))
+    assert rel64 < 1e-4 and rel32 > 0.5, (rel64, rel32)
+
+
+def test_f64_deterministic():
+    M, N, K = 128, 3072, 8192
+    X = dev(WL.gen_x(M, K, seed=3))
+    Wd = dev_w(WL.gen_w(N, K, seed=10), "bf16")
+    C = sp.correction_f64(Wd, M, G, DELTA_ACT, 1.0, 0, 9, 0)
+    a = host(sp.masked_linear_fused_f64(X, Wd, C, G, DELTA_ACT, 1.0, 0, 9, 0))
+    b = host(sp.masked_linear_fused_f64(X, Wd, C, G, DELTA_ACT, 1.0, 0, 9, 0))
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
