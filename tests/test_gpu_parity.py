@@ -250,7 +250,7 @@ def test_fused_within_theorem4_gate(prec, mech, M, N, K, delta, eps):
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
 @pytest.mark.parametrize("M", [1, 4, 16])
-@pytest.mark.parametrize("N,K", [(6144, 2560), (200, 9728), (40, 264)])
+@pytest.mark.parametrize("N,K", [(6144, 2560), (200, 9728), (40, 264), (72, 16400)])
 def test_fused_skinny_decode(prec, M, N, K):
     err, b, _, _ = _fused_case(M, N, K, "gaussian", 719.8, 2.0, prec, row0=1000 + M)
     assert np.all(err <= b["gate"])
@@ -258,7 +258,7 @@ def test_fused_skinny_decode(prec, M, N, K):
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
 @pytest.mark.parametrize("M", [1, 2, 3, 16])
-@pytest.mark.parametrize("N,K,xpad", [(6144, 2560, 0), (200, 9728, 8), (40, 264, 0)])
+@pytest.mark.parametrize("N,K,xpad", [(6144, 2560, 0), (200, 9728, 8), (40, 264, 0), (72, 16400, 0)])
 def test_fused_precomputed_mask_is_the_two_launch_path(prec, M, N, K, xpad):
     # decode with a precomputed mask forms fl32(X + eta) inside the GEMM: bit for
     # bit the mask kernel followed by the GEMM, and the in-stream-noise fused call
