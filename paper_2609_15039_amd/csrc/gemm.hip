@@ -1097,16 +1097,15 @@ gemv_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float*
 
 // GEMV with K split over the waves (K <= 16384 and fewer than GS_MAX_PAIRS row pairs;
 // the kernel above serves longer rows and the widest N).
-// A workgroup owns GS_ROWS W rows; wave w takes the 512-k chunks j = w, w + 4, .. of
-// each row, issues all of its W loads at once, forms
+// A workgroup owns GS_ROWS (4 or 5) W rows; wave w takes the 512-k chunks j = w, w + 4, ..
+// of each row, issues all of its W loads at once, forms
 // the masked input of its own chunks in registers (from X + eta or from the
 // planes, exactly as above), accumulates fma(x~, w, acc) in chunk and k order,
 // sums its lanes with the same butterfly, and the four waves' sums are added in
 // wave order.
 constexpr int GS_MAX_CH = 8;  // chunks per wave: K <= 4 x 8 x 512
-constexpr int GS_ROWS = 4;    // W rows per workgroup
 
-template <int NPL, bool MASK, int MR, int CH>
+template <int NPL, bool MASK, int MR, int CH, int GS_ROWS>
 __global__ void __launch_bounds__(GV_WAVES * WAVE)
 gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C,
                   int64_t ldc, float* __restrict__ Out, int64_t ldo, int N, int K)
@@ -1325,20 +1324,36 @@ Plan plan_skinny(int64_t M, int64_t N, int64_t K, int prec)
     return p;
 }
 
-// GS_ROWS rows per workgroup, K split over its waves: measured on the Qwen3-4B decode
-// projections (N 2560 .. 19456) 10-40% faster than the streaming GEMV, and 1-3% slower
-// on the LM heads (N 128256, 151936), which keep the streaming kernel; 4 rows per
-// workgroup beat 1, 2 and 8.
+// K split over the waves of a workgroup: measured on the Qwen3-4B decode projections
+// (N 2560 .. 19456) 10-40% faster than the streaming GEMV, and 1-3% slower on the LM
+// heads (N 128256, 151936), which keep the streaming kernel.  Rows per workgroup: 4 or
+// 5, whichever gives the busiest CU (256 CUs, workgroups dealt out evenly) the fewest
+// rows, 4 on a tie (4 beat 1, 2 and 8 rows at N = 2560, 6144 and 19456).
 constexpr int64_t GS_MAX_PAIRS = 32768;
+
+int gs_rows(int64_t N)
+{
+    auto busiest = [&](int64_t r) { return ((N + r - 1) / r + 255) / 256 * r; };
+    return busiest(5) < busiest(4) ? 5 : 4;
+}
 
 template <bool MASK>
 int launch_gemv_split(const SkSrc& src, int prec, const void* W, int64_t ldw, const float* C, int64_t ldc,
                       float* Out, int64_t ldo, int64_t M, int64_t N, int64_t K, hipStream_t s)
 {
     const int ch = (int)(((K + 511) / 512 + GV_WAVES - 1) / GV_WAVES);
-    const dim3 grid((unsigned)((N + GS_ROWS - 1) / GS_ROWS));
+    const int rows = gs_rows(N);
+    const dim3 grid((unsigned)((N + rows - 1) / rows));
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
-#define GS_LAUNCH(NP, MR, CHN) hipLaunchKernelGGL((gemv_split_kernel<NP, MASK, MR, CHN>), grid, dim3(GV_WAVES * WAVE), 0, s, src, w, ldw, C, ldc, Out, ldo, (int)N, (int)K)
+#define GS_LAUNCH(NP, MR, CHN)                                                                                      \
+    do {                                                                                                            \
+        if (rows == 5)                                                                                              \
+            hipLaunchKernelGGL((gemv_split_kernel<NP, MASK, MR, CHN, 5>), grid, dim3(GV_WAVES * WAVE), 0, s, src, w, \
+                               ldw, C, ldc, Out, ldo, (int)N, (int)K);                                              \
+        else                                                                                                        \
+            hipLaunchKernelGGL((gemv_split_kernel<NP, MASK, MR, CHN, 4>), grid, dim3(GV_WAVES * WAVE), 0, s, src, w, \
+                               ldw, C, ldc, Out, ldo, (int)N, (int)K);                                              \
+    } while (0)
 #define GS_CH(NP, MR)                                                                        \
     switch (ch) {                                                                            \
     case 1: GS_LAUNCH(NP, MR, 1); break;                                                     \
