@@ -14,7 +14,8 @@
  *   X    M x K float32, leading dimension ldx  -- tokens x in-features
  *   eta  M x K float32 (same shape as X)
  *   W    N x K, float32 or bfloat16, ldw       -- out x in (the paper's d' x d
- *                                                 matrix acting on column vectors)
+ *                                                 matrix acting on column vectors),
+ *        or bfloat16 in the tiled order below (SPLITEE_BF16_TILED; ldw unused)
  *   R, C, Y  M x N float32                     -- Y = X W^T
  *
  * Ownership: every pointer is a device pointer owned by the caller; the library
@@ -77,7 +78,7 @@
 extern "C" {
 #endif
 
-#define SPLITEE_ABI_VERSION 1
+#define SPLITEE_ABI_VERSION 2
 
 typedef enum {
     SPLITEE_OK = 0,
@@ -95,7 +96,7 @@ typedef enum {
 } splitee_status;
 
 typedef enum { SPLITEE_MECH_LAPLACE = 0, SPLITEE_MECH_GAUSSIAN = 1, SPLITEE_MECH_NONE = 2 } splitee_mech;
-typedef enum { SPLITEE_F32 = 0, SPLITEE_BF16 = 1 } splitee_dtype;
+typedef enum { SPLITEE_F32 = 0, SPLITEE_BF16 = 1, SPLITEE_BF16_TILED = 2 } splitee_dtype;
 typedef enum {
     SPLITEE_PREC_F32 = 0,
     SPLITEE_PREC_BF16 = 1,
@@ -169,10 +170,36 @@ int splitee_noise_mask(const float* X, int64_t ldx, void* Xt, int out_prec, int6
                        uint64_t stream_id, uint64_t row0, void* stream);
 
 /*
+ * Tiled weight order (SPLITEE_BF16_TILED).  The projection weights are fixed for
+ * the life of a model, so they can be stored once in the order the MFMA kernels
+ * load them: every 16-byte load of a wavefront then covers whole 128-byte cache
+ * lines (row-major W gives 32 rows x 32 bytes per load, a quarter of the vector L1
+ * bandwidth).  With N32 = ceil(N / 32) 32-row blocks and KT = ceil(K / 64) 64-wide k
+ * tiles, bfloat16 element W[n][k] sits at element index
+ *     ((((n / 32) KT + k / 64) 4 + (k % 64) / 16) 64 + ((k % 16) / 8) 32 + n % 32) 8 + k % 8
+ * of an N32 x KT x 4096-byte buffer; rows n >= N and columns k >= K are zeros.
+ * Accepted by splitee_masked_linear, splitee_masked_linear_unmask,
+ * splitee_masked_linear_fused and splitee_correction with BF16 / BF16X3 precision
+ * (SPLITEE_ERR_UNSUPPORTED with F32, in the binary64 calls and splitee_spectral_norm);
+ * the result equals the row-major call's within the same error bounds (the kernels
+ * and their K splits differ, so the summation order may too).
+ */
+size_t splitee_tiled_weights_bytes(int64_t N, int64_t K); /* 0 on invalid N, K (K % 8 != 0) */
+
+/*
+ * Writes W (N x K bfloat16, row-major, ldw >= K, 16-byte aligned rows) into Wt in
+ * the tiled order, splitee_tiled_weights_bytes(N, K) bytes (caller-owned, 16-byte
+ * aligned, must not overlap W: SPLITEE_ERR_ARG).  Requires K % 8 == 0.  A copy:
+ * every byte of W reaches Wt unchanged.
+ */
+int splitee_tile_weights(const void* W, int64_t ldw, int64_t N, int64_t K, void* Wt, void* stream);
+
+/*
  * The GPU's part of the method: R = Xt W^T (r = W (x + eta), Sec. "Offloading
  * Linear Operations"), with float32 accumulation.
  *   Xt     in_prec operand as written by splitee_mask (ldxt)
- *   W      N x K, w_type float32 or bfloat16 (ldw); BF16 / BF16X3 need bfloat16 W
+ *   W      N x K, w_type float32, bfloat16 (ldw) or tiled bfloat16; BF16 / BF16X3 need
+ *          bfloat16 W, F32 takes row-major W
  *   R      out, M x N float32 (ldr)
  * Requires K % 8 == 0.  Needs no workspace (single-pass K reduction per tile).
  */
@@ -188,15 +215,16 @@ int splitee_unmask(const float* R, int64_t ldr, const float* C, int64_t ldc, flo
                    int64_t M, int64_t N, void* stream);
 
 /* Workspace bytes needed by splitee_masked_linear_unmask for this shape and
- * precision (split-K counters and partial tiles); 0 when none is needed. */
+ * precision (split-K counters and partial tiles), enough for either weight
+ * layout; 0 when none is needed. */
 size_t splitee_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
 
 /*
  * GEMM with the unmask epilogue: Y = fl32(fl(Xt W^T) - C) (C NULL: Y = R), the
  * second half of splitee_masked_linear_fused.  Xt as written by splitee_mask or
  * splitee_noise_mask (ldxt, planes M * ldxt apart).  Small tile counts are split
- * over K; the partial tiles are summed in a fixed order by the last workgroup of
- * each tile, so results are deterministic.  workspace: >=
+ * over K; the partial tiles are summed in split order (by a second kernel, or by
+ * the last workgroup of each tile), so results are deterministic.  workspace: >=
  * splitee_gemm_workspace_bytes bytes, 256-byte aligned, zero-filled before its
  * first use (calls leave it zeroed).  Requires K % 8 == 0.
  */
@@ -206,7 +234,8 @@ int splitee_masked_linear_unmask(const void* Xt, int in_prec, int64_t ldxt, cons
                                  size_t workspace_bytes, void* stream);
 
 /* Workspace bytes needed by splitee_masked_linear_fused (and splitee_correction)
- * for this shape and precision; 0 on invalid arguments. */
+ * for this shape and precision, enough for either weight layout; 0 on invalid
+ * arguments. */
 size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
 
 /*
@@ -218,9 +247,10 @@ size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
  * noise arguments are then only validated.  C (M x N, ldc) must be the correction
  * of the same mask, e.g. from splitee_correction with the same noise arguments; for
  * a decode step at positions [t, t+M) pass row0 = t and C = bank + t * ldc.
- * M <= 16 with BF16 or BF16X3 takes the skinny bandwidth-bound kernel (decode);
- * given eta_override it forms fl32(X + eta) and its bfloat16 planes inside that
- * kernel (one launch, bit-identical to the two-launch path).  Otherwise the tiled
+ * M <= 16 with BF16 or BF16X3 takes the bandwidth-bound decode kernels (M <= 2
+ * with row-major W: a vector-ALU GEMV; otherwise the skinny MFMA kernel); given
+ * eta_override they form fl32(X + eta) and its bfloat16 planes themselves (one
+ * launch, bit-identical to the two-launch path).  Otherwise the tiled
  * or W-streamed MFMA kernel runs, split over K when the tile count is small.
  * workspace: >= splitee_fused_workspace_bytes(M, N, K, prec) bytes, 256-byte
  * aligned; it must hold zeros before its first use and calls leave it that way.

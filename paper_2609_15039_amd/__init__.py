@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libsplitee.so")
 
 SPLITEE_OK = 0
 SPLITEE_MECH_LAPLACE, SPLITEE_MECH_GAUSSIAN, SPLITEE_MECH_NONE = 0, 1, 2
-SPLITEE_F32, SPLITEE_BF16 = 0, 1
+SPLITEE_F32, SPLITEE_BF16, SPLITEE_BF16_TILED = 0, 1, 2
 SPLITEE_PREC_F32, SPLITEE_PREC_BF16, SPLITEE_PREC_BF16X3 = 0, 1, 2
 MECHS = {"laplace": SPLITEE_MECH_LAPLACE, "gaussian": SPLITEE_MECH_GAUSSIAN, "none": SPLITEE_MECH_NONE}
 PRECS = {"f32": SPLITEE_PREC_F32, "bf16": SPLITEE_PREC_BF16, "bf16x3": SPLITEE_PREC_BF16X3}
@@ -32,6 +32,7 @@ EXPORTED = [
     "splitee_bank_path", "splitee_bank_workspace_bytes", "splitee_bank_create", "splitee_bank_open",
     "splitee_bank_info", "splitee_bank_load", "splitee_bank_close",
     "splitee_f64_workspace_bytes", "splitee_masked_linear_fused_f64", "splitee_correction_f64",
+    "splitee_tiled_weights_bytes", "splitee_tile_weights",
 ]
 SPLITEE_PREC_F64 = 3
 SPLITEE_ERR_IO, SPLITEE_ERR_EXHAUSTED, SPLITEE_ERR_FORMAT, SPLITEE_ERR_BUSY = -8, -9, -10, -11
@@ -103,6 +104,8 @@ def load():
         "splitee_masked_linear_fused_f64": (I, [P, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, I, D, D, U64,
                                                 U64, U64, P, SZ, P]),
         "splitee_correction_f64": (I, [P, I64, P, I, I64, I64, I64, I64, I, D, D, U64, U64, U64, P, SZ, P]),
+        "splitee_tiled_weights_bytes": (SZ, [I64, I64]),
+        "splitee_tile_weights": (I, [P, I64, I64, I64, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -142,7 +145,38 @@ def _check(fn, status):
         raise SpliteeError(fn, status)
 
 
+class TiledWeights:
+    """A bfloat16 N x K weight matrix stored in the tiled order of
+    splitee_tile_weights (`data`, a flat device tensor).  Passed wherever a W tensor
+    is taken; shape, dtype, stride and data_ptr describe the logical matrix."""
+
+    dtype = torch.bfloat16
+
+    def __init__(self, data, N, K):
+        self.data, self.N, self.K = data, N, K
+
+    @property
+    def shape(self):
+        return (self.N, self.K)
+
+    @property
+    def device(self):
+        return self.data.device
+
+    @property
+    def is_cuda(self):
+        return self.data.is_cuda
+
+    def stride(self, dim):
+        return (self.K, 1)[dim]
+
+    def data_ptr(self):
+        return self.data.data_ptr()
+
+
 def _wtype(W):
+    if isinstance(W, TiledWeights):
+        return SPLITEE_BF16_TILED
     return SPLITEE_BF16 if W.dtype == torch.bfloat16 else SPLITEE_F32
 
 
@@ -154,6 +188,14 @@ def splitee_abi_version():
 
 def splitee_status_string(status):
     return load().splitee_status_string(status).decode()
+
+
+def splitee_tiled_weights_bytes(N, K):
+    return load().splitee_tiled_weights_bytes(N, K)
+
+
+def splitee_tile_weights(W, ldw, N, K, Wt, stream=None):
+    _check("splitee_tile_weights", load().splitee_tile_weights(_ptr(W), ldw, N, K, _ptr(Wt), _stream(stream)))
 
 
 def splitee_noise_gen(eta, ld_eta, M, K, mech, sensitivity, epsilon, seed, stream_id, row0=0,
@@ -412,6 +454,14 @@ def workspace(M, N, K, prec, device="cuda", gemm_only=False):
     ws = torch.zeros(max(nbytes, 1) + 256, dtype=torch.uint8, device=device)
     off = (-ws.data_ptr()) % 256
     return ws[off:off + max(nbytes, 1)], nbytes
+
+
+def tile_weights(W):
+    """W (N x K bfloat16, row-major) in the tiled order, as TiledWeights."""
+    N, K = W.shape
+    data = torch.empty(splitee_tiled_weights_bytes(N, K) // 2, dtype=torch.bfloat16, device=W.device)
+    splitee_tile_weights(W, W.stride(0), N, K, data)
+    return TiledWeights(data, N, K)
 
 
 def noise(M, K, mech, sensitivity, epsilon, seed, stream_id, row0=0, device="cuda"):

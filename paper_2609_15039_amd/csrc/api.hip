@@ -43,7 +43,7 @@ inline bool valid_prec(int prec)
 {
     return prec == SPLITEE_PREC_F32 || prec == SPLITEE_PREC_BF16 || prec == SPLITEE_PREC_BF16X3;
 }
-inline bool valid_dtype(int t) { return t == SPLITEE_F32 || t == SPLITEE_BF16; }
+inline bool valid_dtype(int t) { return t == SPLITEE_F32 || t == SPLITEE_BF16 || t == SPLITEE_BF16_TILED; }
 
 // Skinny kernel for decode-sized M with bfloat16 operands, tiled kernel otherwise.
 inline bool use_skinny(int64_t M, int prec) { return M <= 16 && prec != SPLITEE_PREC_F32; }
@@ -52,6 +52,14 @@ size_t gemm_ws(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
     return use_skinny(M, prec) ? splitee_host::skinny_workspace_bytes(M, N, K, prec)
                                : splitee_host::gemm_workspace_bytes(M, N, K, prec, w_type);
+}
+// Workspace queries take no weight layout: the larger of the row-major and the
+// tiled plan (the float32 MFMA path reads row-major W only).
+size_t gemm_ws_any(int64_t M, int64_t N, int64_t K, int prec)
+{
+    const size_t a = gemm_ws(M, N, K, prec, SPLITEE_BF16);
+    const size_t b = prec == SPLITEE_PREC_F32 ? 0 : gemm_ws(M, N, K, prec, SPLITEE_BF16_TILED);
+    return a > b ? a : b;
 }
 size_t gemm_counters(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
@@ -63,6 +71,10 @@ size_t gemm_counters(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 int check_w(const void* W, int w_type, int64_t ldw, int64_t K, int prec)
 {
     if (!valid_dtype(w_type)) return SPLITEE_ERR_DTYPE;
+    if (w_type == SPLITEE_BF16_TILED) { // ldw is not used: the layout is fixed by N and K
+        if (prec == SPLITEE_PREC_F32) return SPLITEE_ERR_UNSUPPORTED;
+        return aligned16(W) ? SPLITEE_OK : SPLITEE_ERR_ALIGN;
+    }
     if (prec != SPLITEE_PREC_F32 && w_type != SPLITEE_BF16) return SPLITEE_ERR_UNSUPPORTED;
     const int64_t wes = w_type == SPLITEE_F32 ? 4 : 2;
     if (ldw < K) return SPLITEE_ERR_SHAPE;
@@ -76,7 +88,7 @@ int run_gemm(const void* Xt, int prec, int64_t ldxt, const void* W, int w_type, 
              void* ws, size_t ws_bytes, hipStream_t s)
 {
     if (use_skinny(M, prec))
-        return splitee_host::launch_skinny(Xt, prec, ldxt, M * ldxt, W, ldw, C, ldc, Y, ldy, M, N, K, ws,
+        return splitee_host::launch_skinny(Xt, prec, ldxt, M * ldxt, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, ws,
                                            ws_bytes, s);
     return splitee_host::launch_gemm(Xt, prec, ldxt, M * ldxt, W, w_type, ldw, C, ldc, Y, ldy, M, N, K,
                                      ws, ws_bytes, s);
@@ -97,7 +109,7 @@ int run_masked(const float* X, int64_t ldx, const void* W, int w_type, int64_t l
     char* base = reinterpret_cast<char*>(ws);
     if (eta_override && use_skinny(M, prec))
         // decode with a precomputed mask: the GEMM forms fl32(X + eta) itself
-        return splitee_host::launch_skinny_masked(X, ldx, eta_override, K, prec, W, ldw, C, ldc, Y, ldy, M, N,
+        return splitee_host::launch_skinny_masked(X, ldx, eta_override, K, prec, W, w_type, ldw, C, ldc, Y, ldy, M, N,
                                                   K, base, gws, s);
     void* Xt = base + gws;
     unsigned* counters = reinterpret_cast<unsigned*>(base);
@@ -137,6 +149,7 @@ int run_f64(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
 int check_w_f64(const void* W, int w_type, int64_t ldw, int64_t K)
 {
     if (!valid_dtype(w_type)) return SPLITEE_ERR_DTYPE;
+    if (w_type == SPLITEE_BF16_TILED) return SPLITEE_ERR_UNSUPPORTED;
     if (ldw < K) return SPLITEE_ERR_SHAPE;
     if (!aligned16(W) || !pitch16(ldw, w_type == SPLITEE_F32 ? 4 : 2)) return SPLITEE_ERR_ALIGN;
     return SPLITEE_OK;
@@ -147,6 +160,26 @@ int check_w_f64(const void* W, int w_type, int64_t ldw, int64_t K)
 extern "C" {
 
 int splitee_abi_version(void) { return SPLITEE_ABI_VERSION; }
+
+size_t splitee_tiled_weights_bytes(int64_t N, int64_t K)
+{
+    if (!dims_ok(0, N, K) || K % 8 != 0) return 0;
+    return splitee::tiled_weights_bytes(N, K);
+}
+
+int splitee_tile_weights(const void* W, int64_t ldw, int64_t N, int64_t K, void* Wt, void* stream)
+{
+    if (!dims_ok(0, N, K) || K % 8 != 0 || ldw < K) return SPLITEE_ERR_SHAPE;
+    if (N == 0 || K == 0) return SPLITEE_OK;
+    if (!W || !Wt) return SPLITEE_ERR_ARG;
+    if (!aligned16(W) || !pitch16(ldw, 2) || !aligned16(Wt)) return SPLITEE_ERR_ALIGN;
+    const char* a = reinterpret_cast<const char*>(W);
+    const char* b = reinterpret_cast<const char*>(Wt);
+    const size_t in_bytes = (size_t)((N - 1) * ldw + K) * 2, out_bytes = splitee::tiled_weights_bytes(N, K);
+    if (a < b + out_bytes && b < a + in_bytes) return SPLITEE_ERR_ARG; // in place is not supported
+    return splitee_host::launch_tile_weights(reinterpret_cast<const uint16_t*>(W), ldw, N, K,
+                                             reinterpret_cast<uint16_t*>(Wt), as_stream(stream));
+}
 
 const char* splitee_status_string(int status)
 {
@@ -270,7 +303,7 @@ int splitee_unmask(const float* R, int64_t ldr, const float* C, int64_t ldc, flo
 size_t splitee_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
 {
     if (!valid_prec(prec) || !dims_ok(M, N, K) || K % 8 != 0) return 0;
-    return gemm_ws(M, N, K, prec, SPLITEE_BF16);
+    return gemm_ws_any(M, N, K, prec);
 }
 
 int splitee_masked_linear_unmask(const void* Xt, int in_prec, int64_t ldxt, const void* W,
@@ -297,8 +330,7 @@ int splitee_masked_linear_unmask(const void* Xt, int in_prec, int64_t ldxt, cons
 size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
 {
     if (!valid_prec(prec) || !dims_ok(M, N, K) || K % 8 != 0) return 0;
-    const int w_type = SPLITEE_BF16;
-    return align256(gemm_ws(M, N, K, prec, w_type)) +
+    return align256(gemm_ws_any(M, N, K, prec)) +
            align256((size_t)(prec_planes(prec) * M * K * prec_elsize(prec)));
 }
 
@@ -405,6 +437,7 @@ int splitee_spectral_norm(const void* W, int w_type, int64_t ldw, int64_t N, int
                           void* workspace, size_t workspace_bytes, void* stream)
 {
     if (!valid_dtype(w_type)) return SPLITEE_ERR_DTYPE;
+    if (w_type == SPLITEE_BF16_TILED) return SPLITEE_ERR_UNSUPPORTED;
     if (iters < 1 || iters > MAX_POWER_ITERS || !sigma) return SPLITEE_ERR_ARG;
     if (!dims_ok(0, N, K) || K % 8 != 0 || ldw < K) return SPLITEE_ERR_SHAPE;
     if (K > splitee_host::spectral_max_k()) return SPLITEE_ERR_UNSUPPORTED;

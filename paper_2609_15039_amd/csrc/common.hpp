@@ -14,6 +14,13 @@ namespace splitee {
 // most noise blocks one splitee_noise_gen_multi call generates
 constexpr int NOISE_MULTI_MAX = 8;
 
+// Bytes of a bfloat16 N x K weight matrix in the tiled order: 32-row blocks of
+// 64-k tiles, 4 KB each, N padded to a multiple of 32 and K to a multiple of 64.
+inline size_t tiled_weights_bytes(int64_t N, int64_t K)
+{
+    return (size_t)((N + 31) / 32) * (size_t)((K + 63) / 64) * 4096u;
+}
+
 // binary32 -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
 __device__ __forceinline__ uint32_t bf16_bits_rne(float x)
 {
@@ -71,12 +78,14 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t plane_stride, cons
 // Decode GEMM whose masked input fl32(X + eta) is formed in-kernel from X and a
 // given mask eta (both M x K float32).
 int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec,
-                         const void* W, int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo,
-                         int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+                         const void* W, int w_type, int64_t ldw, const float* C, int64_t ldc, float* Out,
+                         int64_t ldo, int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
 size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
-int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W,
+int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W, int w_type,
                   int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,
                   int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+// bfloat16 W (N x K, row-major) -> the tiled order (splitee_tile_weights).
+int launch_tile_weights(const uint16_t* W, int64_t ldw, int64_t N, int64_t K, uint16_t* Wt, hipStream_t s);
 // Binary64 GEMM Out = A W^T (- C), A binary64, W bf16 / f32, Out binary64 or rounded to binary32.
 size_t f64_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 int launch_gemm_f64(const double* A, int64_t lda, const void* W, int w_type, int64_t ldw, const double* C,

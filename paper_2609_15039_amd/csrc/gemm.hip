@@ -251,6 +251,14 @@ __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff)
 // Split over K, each workgroup writes its partial accumulators in register
 // order (16-byte stores, no atomics) and `stream_sum_kernel` adds the splits in
 // split order and applies the unmask epilogue.
+//
+// W in row-major order: lane (c, h) of a B-operand load reads 16 bytes of row c
+// of a 32-row block, so one load touches 32 cache lines for 32 bytes each, and the
+// vector L1 (which serves a 128-byte line access every other clock, however few
+// bytes of it are used) delivers a quarter of its bandwidth.  W in the tiled order
+// (TILED; splitee_tile_weights) stores each (32-row block, K tile, k step) as the
+// 1 KB the 64 lanes load, so every load is 8 whole lines.  With tiled W the kernel
+// runs 8 waves (two per SIMD): one wave's MFMAs overlap the other's load issue.
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -284,14 +292,14 @@ __device__ __forceinline__ int lds_swizzle(int r)
     return SW == 0 ? (r & 7) : ((r >> 1) & 7);
 }
 
-template <int NPL, int BM, int BN, int WGM, int D, int SW = 1>
-__global__ void __launch_bounds__(ST_NW * WAVE)
+template <int NPL, int BM, int BN, int WGM, int D, int NW = ST_NW, bool TILED = false, int SW = 1>
+__global__ void __launch_bounds__(NW * WAVE)
 gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
                    const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
                    float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
                    int ksplit, int kt_per_split, float* __restrict__ part)
 {
-    constexpr int NW = ST_NW, WGN = NW / WGM;
+    constexpr int WGN = NW / WGM;
     constexpr int WTM = BM / WGM, WTN = BN / WGN; // wave tile
     constexpr int TM = WTM / 32, TN = WTN / 32;   // 32 x 32 MFMA blocks of the wave tile
     constexpr int S = D + 1;                  // masked-input stages = W register slots
@@ -318,7 +326,8 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     const int nloop = (nk + S - 1) / S * S; // whole turns of the ring; tiles past kt1 read zeros
 
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(W, (uint32_t)(TILED ? (int64_t)((N + 31) / 32) * ktiles * 4096 : (int64_t)N * ldw * 2));
 
     // masked input: DMA load t of this wave fills 1 KB = stage rows 8j..8j+7 (j = wave + NW t);
     // lane l writes unit 64j + l: row u / 8, slot u % 8 holding k chunk slot ^ (row & 7)
@@ -332,13 +341,17 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
         akc[t] = kc * 8;
         aoff[t] = gm < M ? (uint32_t)((p * pstride + (int64_t)gm * lda) * 2 + kc * 16) : OOB;
     }
-    // W: lane (c = l % 32, h = l / 32) loads row n0 + WTN wn + 32 j + c, 16 bytes at k = 16 s + 8 h
+    // W: lane (c = l % 32, h = l / 32) loads row n0 + WTN wn + 32 j + c, 16 bytes at k = 16 s + 8 h;
+    // tiled, that is byte 16 l of the k step's 1 KB in block ((n0 + WTN wn + 32 j) / 32, K tile)
     const int fc = lane % 32, fh = lane / 32;
     uint32_t woff[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int gn = n0 + wn * WTN + j * 32 + fc;
-        woff[j] = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fh * 16) : OOB;
+        if (TILED)
+            woff[j] = gn < N ? (uint32_t)((int64_t)(gn / 32) * ktiles * 4096 + lane * 16) : OOB;
+        else
+            woff[j] = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fh * 16) : OOB;
     }
 
     unsigned char* const st0 = stream_stage<0, SB>();
@@ -368,8 +381,13 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
         }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const bool ok = live && woff[j] != OOB && kb + 16 * part + 8 * fh < K;
-            wb[q][j][part] = load16(rw, ok ? woff[j] + (uint32_t)(kb + 16 * part) * 2 : OOB);
+            if (TILED) { // k past K is zero padding of the tiled layout
+                const bool ok = live && woff[j] != OOB;
+                wb[q][j][part] = load16(rw, ok ? woff[j] + (uint32_t)(kt * 4 + part) * 1024 : OOB);
+            } else {
+                const bool ok = live && woff[j] != OOB && kb + 16 * part + 8 * fh < K;
+                wb[q][j][part] = load16(rw, ok ? woff[j] + (uint32_t)(kb + 16 * part) * 2 : OOB);
+            }
         }
     };
     auto issue = [&](int t, auto sc) {
@@ -482,7 +500,7 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
 // unmask epilogue.  Thread u handles one float4 of one wave's partial (the
 // register order the partials were written in): rows 8 c + 4 (l / 32) + 0..3 of
 // block (i, j), column l % 32.
-template <int BM, int BN, int WGM, int WGN = ST_NW / WGM>
+template <int BM, int BN, int WGM, int WGN>
 __global__ void __launch_bounds__(256)
 stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __restrict__ C, int64_t ldc,
                   float* __restrict__ Out, int64_t ldo, int M, int N, int mtiles, int tiles)
@@ -715,7 +733,7 @@ __device__ __forceinline__ void planes_of(const float (&x)[8], uint4 (&q)[NPL])
     }
 }
 
-template <int NPL, int R, bool MASK>
+template <int NPL, int R, bool MASK, bool TILED = false>
 __global__ void __launch_bounds__(256)
 skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
               float* __restrict__ Out, int64_t ldo, int M, int N, int K, int ntiles, int ksplit,
@@ -734,13 +752,22 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
     const int RS = SA * 64 + 16;                      // LDS row pitch; 16 bytes of padding
     const int fr = lane % 16, fq = lane / 16;
 
-    // the W ring
+    // the W ring.  Lane (r, q) loads row gn = n0 + 16 wave + r, 16 bytes at k = 32 J + 8 q
+    // of k step J.  Tiled (32-row blocks of 64-k tiles, 1 KB per 16-k step, 16 bytes per
+    // (k half h, row c) at (32 h + c) 16), that chunk sits at block (gn / 32, J / 2),
+    // step 2 (J % 2) + q / 2, half q % 2: a constant per lane plus 2048 J, and the 64 lanes
+    // read four 256-byte runs (whole cache lines)
     const int gn = n0 + wave * 16 + fr;
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
-    const uint32_t wbase = gn < N ? (uint32_t)((int64_t)gn * ldw * 2 + fq * 16) : OOB;
+    const int kt64 = (K + 63) / 64;
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(W, (uint32_t)(TILED ? (int64_t)((N + 31) / 32) * kt64 * 4096 : (int64_t)N * ldw * 2));
+    const uint32_t wbase = gn >= N ? OOB
+                           : TILED ? (uint32_t)((int64_t)(gn / 32) * kt64 * 4096 + (fq / 2) * 1024 +
+                                                ((fq % 2) * 32 + gn % 32) * 16)
+                                   : (uint32_t)((int64_t)gn * ldw * 2 + fq * 16);
     auto wload = [&](int j) {
         const bool ok = wbase != OOB && j < ns && (s0 + j) * 32 + fq * 8 < K;
-        return load16(rw, ok ? wbase + (uint32_t)(s0 + j) * 64 : OOB);
+        return load16(rw, ok ? wbase + (uint32_t)(s0 + j) * (TILED ? 2048 : 64) : OOB);
     };
     uint4 ring[R];
 
@@ -1230,20 +1257,34 @@ constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 //   M <= 64:       64 x 256, 4 waves side by side  (variants 11 bf16x3, 13 bf16)
 //   64 < M <= 128: 128 x 128, 2 x 2 waves          (variants 14 bf16x3, 15 bf16)
 //   M > 128:       128 x 256, 4 waves side by side (variants 10 bf16x3, 12 bf16)
+// With tiled W, 8 waves per workgroup, measured on the same projections and the
+// Qwen3-4B ones at 1024 tokens:
+//   M <= 64:       64 x 256, 8 waves side by side        (variants 24 bf16x3, 25 bf16)
+//   64 < M <= 128: 128 x 128, 2 x 4 waves                (variants 20, 21), or
+//                  128 x 256 when N has 128 or more 128-column tiles (variants 22, 23)
+//   M > 128:       128 x 256, 2 x 4 waves                (variants 22, 23)
 // The K split fills about 256 CUs, keeps at least ST_MIN_KT K tiles per split and
 // at most ST_MAX_KS splits.
 
 bool use_stream(int prec, int w_type)
 {
-    return prec != SPLITEE_PREC_F32 && w_type == SPLITEE_BF16;
+    return prec != SPLITEE_PREC_F32 && (w_type == SPLITEE_BF16 || w_type == SPLITEE_BF16_TILED);
 }
 
-Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, bool allow_split)
+Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allow_split)
 {
     Plan p{};
     const bool x3 = prec == SPLITEE_PREC_BF16X3;
     p.bk = 64;
-    if (M <= 64) {
+    if (w_type == SPLITEE_BF16_TILED) {
+        if (M <= 64) {
+            p.bm = 64; p.bn = 256; p.variant = x3 ? 24 : 25;
+        } else if (M <= 128 && (N + 127) / 128 < 128) {
+            p.bm = 128; p.bn = 128; p.variant = x3 ? 20 : 21;
+        } else {
+            p.bm = 128; p.bn = 256; p.variant = x3 ? 22 : 23;
+        }
+    } else if (M <= 64) {
         p.bm = 64; p.bn = 256; p.variant = x3 ? 11 : 13;
     } else if (M <= 128) {
         p.bm = 128; p.bn = 128; p.variant = x3 ? 14 : 15;
@@ -1270,7 +1311,7 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, bool allow_split)
 
 Plan plan_tiled(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool allow_split)
 {
-    if (use_stream(prec, w_type)) return plan_stream(M, N, K, prec, allow_split);
+    if (use_stream(prec, w_type)) return plan_stream(M, N, K, prec, w_type, allow_split);
     Plan p{}; // float32 MFMA
     p.bm = 128; p.bn = 128; p.bk = 32; p.variant = 0;
     if (M <= 64) { p.bm = 64; p.bn = 64; p.variant = 1; }
@@ -1394,9 +1435,38 @@ int launch_gemv(const SkSrc& src, int prec, const void* W, int64_t ldw, const fl
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
+// ------------------------------------------------------ tiled weight order
+// Thread t writes 16-byte chunk t of the tiled buffer: chunk 64 (4 (B kt64 + kt) + s) + l
+// holds W[32 B + l % 32][64 kt + 16 s + 8 (l / 32) .. + 7] (zeros past N or K).
+__global__ void __launch_bounds__(256) tile_weights_kernel(const uint16_t* __restrict__ W, int64_t ldw, int64_t N,
+                                                           int64_t K, uint16_t* __restrict__ Wt, int64_t chunks)
+{
+    const int64_t kt64 = (K + 63) / 64;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < chunks;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int l = (int)(t % 64);
+        const int64_t rest = t / 64, st = rest % 4, blk = rest / 4;
+        const int64_t kt = blk % kt64, cb = blk / kt64;
+        const int64_t n = 32 * cb + l % 32, k = 64 * kt + 16 * st + 8 * (l / 32);
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (n < N && k < K) v = *reinterpret_cast<const uint4*>(W + n * ldw + k);
+        *reinterpret_cast<uint4*>(Wt + 8 * t) = v;
+    }
+}
+
 }  // namespace
 
 namespace splitee_host {
+
+int launch_tile_weights(const uint16_t* W, int64_t ldw, int64_t N, int64_t K, uint16_t* Wt, hipStream_t s)
+{
+    const int64_t chunks = (int64_t)(splitee::tiled_weights_bytes(N, K) / 16);
+    if (chunks == 0) return SPLITEE_OK;
+    int64_t g = (chunks + 255) / 256;
+    if (g > 256 * 64) g = 256 * 64;
+    hipLaunchKernelGGL(tile_weights_kernel, dim3((unsigned)g), dim3(256), 0, s, W, ldw, N, K, Wt, chunks);
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
 
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
@@ -1439,30 +1509,41 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
         // the buffer loads address each operand with 31-bit byte offsets
         const int64_t planes = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
-        if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
+        const int64_t wbytes = w_type == SPLITEE_BF16_TILED ? (int64_t)splitee::tiled_weights_bytes(N, K) : N * ldw * 2;
+        if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31))
             return SPLITEE_ERR_UNSUPPORTED;
         float* pp = reinterpret_cast<float*>(ws);
-#define ST_LAUNCH(NP, BM_, BN_, WGM_, D_) hipLaunchKernelGGL((gemm_stream_kernel<NP, BM_, BN_, WGM_, D_>), grid, dim3(ST_NW * WAVE), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
+#define ST_LAUNCH(NP, BM_, BN_, WGM_, D_, NW_, T_) hipLaunchKernelGGL((gemm_stream_kernel<NP, BM_, BN_, WGM_, D_, NW_, T_>), grid, dim3(NW_ * WAVE), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
+#define ST_SUM(BM_, BN_, WGM_, WGN_) hipLaunchKernelGGL((stream_sum_kernel<BM_, BN_, WGM_, WGN_>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles)
         switch (p.variant) {
-        case 10: ST_LAUNCH(3, 128, 256, 1, 2); break;
-        case 11: ST_LAUNCH(3, 64, 256, 1, 3); break;
-        case 12: ST_LAUNCH(1, 128, 256, 1, 2); break;
-        case 13: ST_LAUNCH(1, 64, 256, 1, 3); break;
-        case 14: ST_LAUNCH(3, 128, 128, 2, 2); break;
-        default: ST_LAUNCH(1, 128, 128, 2, 2); break;
+        case 10: ST_LAUNCH(3, 128, 256, 1, 2, 4, false); break;
+        case 11: ST_LAUNCH(3, 64, 256, 1, 3, 4, false); break;
+        case 12: ST_LAUNCH(1, 128, 256, 1, 2, 4, false); break;
+        case 13: ST_LAUNCH(1, 64, 256, 1, 3, 4, false); break;
+        case 14: ST_LAUNCH(3, 128, 128, 2, 2, 4, false); break;
+        case 15: ST_LAUNCH(1, 128, 128, 2, 2, 4, false); break;
+        case 20: ST_LAUNCH(3, 128, 128, 2, 2, 8, true); break;
+        case 21: ST_LAUNCH(1, 128, 128, 2, 2, 8, true); break;
+        case 22: ST_LAUNCH(3, 128, 256, 2, 2, 8, true); break;
+        case 23: ST_LAUNCH(1, 128, 256, 2, 2, 8, true); break;
+        case 24: ST_LAUNCH(3, 64, 256, 1, 3, 8, true); break;
+        default: ST_LAUNCH(1, 64, 256, 1, 3, 8, true); break;
         }
-#undef ST_LAUNCH
         if (p.ksplit > 1) {
             const int tiles = p.mtiles * p.ntiles;
             const int64_t units = (int64_t)tiles * p.bm * p.bn / 4; // float4 units of the partial tiles
             const dim3 g2((unsigned)((units + 255) / 256));
-            if (p.variant >= 14)
-                hipLaunchKernelGGL((stream_sum_kernel<128, 128, 2>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
-            else if (p.bm == 128)
-                hipLaunchKernelGGL((stream_sum_kernel<128, 256, 1>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
-            else
-                hipLaunchKernelGGL((stream_sum_kernel<64, 256, 1>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
+            switch (p.variant) {
+            case 10: case 12: ST_SUM(128, 256, 1, 4); break;
+            case 11: case 13: ST_SUM(64, 256, 1, 4); break;
+            case 14: case 15: ST_SUM(128, 128, 2, 2); break;
+            case 20: case 21: ST_SUM(128, 128, 2, 4); break;
+            case 22: case 23: ST_SUM(128, 256, 2, 4); break;
+            default: ST_SUM(64, 256, 1, 8); break;
+            }
         }
+#undef ST_SUM
+#undef ST_LAUNCH
     }
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
@@ -1478,59 +1559,60 @@ size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec)
     return plan_skinny(M, N, K, prec).counter_bytes;
 }
 
-int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const void* W, int64_t ldw,
+// The skinny kernel for one decode GEMM (plan, workspace split, instantiation).
+template <bool MASK>
+int run_skinny(const SkSrc& src, int prec, const void* W, bool tiled, int64_t ldw, const float* C, int64_t ldc,
+               float* Out, int64_t ldo, int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
+    Plan p = plan_skinny(M, N, K, prec);
+    const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
+    if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
+    if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
+    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
+    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
+    dim3 grid((unsigned)(p.ntiles * p.ksplit));
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+#define SK_LAUNCH(NP, T) hipLaunchKernelGGL((skinny_kernel<NP, SK_RING, MASK, T>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters)
+    if (npl == 1) { if (tiled) SK_LAUNCH(1, true); else SK_LAUNCH(1, false); }
+    else { if (tiled) SK_LAUNCH(3, true); else SK_LAUNCH(3, false); }
+#undef SK_LAUNCH
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
+
+// M <= 2 runs on the GEMV kernels with row-major W and on the skinny kernel with
+// tiled W (whose loads the GEMV's whole-row reads do not match).
+int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const void* W, int w_type, int64_t ldw,
                   const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M, int64_t N,
                   int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
 {
     if (M == 0 || N == 0) return SPLITEE_OK;
     if (M > 16 || prec == SPLITEE_PREC_F32) return SPLITEE_ERR_UNSUPPORTED;
     const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
-    if ((npl - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || N * ldw * 2 >= (int64_t(1) << 31))
+    const bool tiled = w_type == SPLITEE_BF16_TILED;
+    const int64_t wbytes = tiled ? (int64_t)splitee::tiled_weights_bytes(N, K) : N * ldw * 2;
+    if ((npl - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31))
         return SPLITEE_ERR_UNSUPPORTED;
     const SkSrc src{reinterpret_cast<const uint16_t*>(A), lda, pstride, nullptr, 0, nullptr, 0};
-    if (M <= GV_MMAX) return launch_gemv<false>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
-    Plan p = plan_skinny(M, N, K, prec);
-    const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
-    if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
-    if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
-    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
-    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
-    dim3 grid((unsigned)(p.ntiles * p.ksplit));
-    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
-    if (prec == SPLITEE_PREC_BF16)
-        hipLaunchKernelGGL((skinny_kernel<1, SK_RING, false>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
-    else
-        hipLaunchKernelGGL((skinny_kernel<3, SK_RING, false>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
-    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+    if (M <= GV_MMAX && !tiled) return launch_gemv<false>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
+    return run_skinny<false>(src, prec, W, tiled, ldw, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s);
 }
 
 int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec,
-                         const void* W, int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo,
-                         int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+                         const void* W, int w_type, int64_t ldw, const float* C, int64_t ldc, float* Out,
+                         int64_t ldo, int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
 {
     if (M == 0 || N == 0) return SPLITEE_OK;
     if (M > 16 || prec == SPLITEE_PREC_F32) return SPLITEE_ERR_UNSUPPORTED;
     if (!X || !eta) return SPLITEE_ERR_ARG;
     if (K % 8 != 0 || ld_eta < K || ldx < K) return SPLITEE_ERR_SHAPE;
-    if (M * ld_eta * 4 >= (int64_t(1) << 31) || M * ldx * 4 >= (int64_t(1) << 31) ||
-        N * ldw * 2 >= (int64_t(1) << 31))
+    const bool tiled = w_type == SPLITEE_BF16_TILED;
+    const int64_t wbytes = tiled ? (int64_t)splitee::tiled_weights_bytes(N, K) : N * ldw * 2;
+    if (M * ld_eta * 4 >= (int64_t(1) << 31) || M * ldx * 4 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31))
         return SPLITEE_ERR_UNSUPPORTED;
-    const int npl = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
     const SkSrc src{nullptr, 0, 0, X, ldx, eta, ld_eta};
-    if (M <= GV_MMAX) return launch_gemv<true>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
-    Plan p = plan_skinny(M, N, K, prec);
-    const size_t lds = skinny_lds_bytes(M, npl, p.kt_per_split);
-    if (lds > (size_t)SK_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
-    if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
-    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
-    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
-    dim3 grid((unsigned)(p.ntiles * p.ksplit));
-    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
-    if (prec == SPLITEE_PREC_BF16)
-        hipLaunchKernelGGL((skinny_kernel<1, SK_RING, true>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
-    else
-        hipLaunchKernelGGL((skinny_kernel<3, SK_RING, true>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters);
-    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+    if (M <= GV_MMAX && !tiled) return launch_gemv<true>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
+    return run_skinny<true>(src, prec, W, tiled, ldw, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s);
 }
 
 }  // namespace splitee_host

@@ -18,7 +18,7 @@ HDR = os.path.join(ROOT, "include", "splitee.h")
 OK, ARG, SHAPE, DTYPE, ALIGN, UNSUP, HIP, WS = 0, -1, -2, -3, -4, -5, -6, -7
 P = 16  # aligned stand-in pointer
 L, G, NONE = 0, 1, 2
-F32, BF16 = 0, 1
+F32, BF16, TILED = 0, 1, 2
 PF, PB, PX = 0, 1, 2
 
 
@@ -41,7 +41,7 @@ def test_library_exports_every_declared_function(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.splitee_abi_version() == 1
+    assert lib.splitee_abi_version() == 2
     for code in (OK, ARG, SHAPE, DTYPE, ALIGN, UNSUP, HIP, WS):
         assert lib.splitee_status_string(code)
     assert lib.splitee_status_string(12345) == b"unknown status"
@@ -164,7 +164,7 @@ def spectral(lib, W=P, wt=BF16, ldw=8, N=4, K=8, iters=3, sigma=True, hist=None,
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(wt=2), DTYPE), (dict(iters=0), ARG), (dict(iters=(1 << 20) + 1), ARG), (dict(sigma=False), ARG),
+    (dict(wt=7), DTYPE), (dict(iters=0), ARG), (dict(iters=(1 << 20) + 1), ARG), (dict(sigma=False), ARG),
     (dict(K=12, ldw=16), SHAPE), (dict(ldw=4), SHAPE), (dict(N=-1), SHAPE), (dict(K=-8), SHAPE),
     (dict(W=None), ARG), (dict(W=8), ALIGN), (dict(ldw=12), ALIGN), (dict(wt=F32, ldw=10, K=8), ALIGN),
     (dict(ws=None), WS), (dict(wsb=16), WS), (dict(ws=16), ALIGN)])
@@ -247,3 +247,55 @@ def test_correction_f64_validation_and_workspace(lib):
     assert q(2, 8, 6) == 0
     assert q(128, 3072, 8192) >= 128 * 8192 * 8  # the binary64 masked input
     assert q(128, 3072, 8192) % 256 == 0
+
+
+# ------------------------------------------------------------ tiled weight order
+
+@pytest.mark.parametrize("N,K", [(1, 8), (32, 64), (33, 64), (200, 264), (5120, 3072), (128256, 3072)])
+def test_tiled_weights_bytes(lib, N, K):
+    # 32-row blocks of 64-k tiles, 4 KB each
+    assert lib.splitee_tiled_weights_bytes(N, K) == -(-N // 32) * -(-K // 64) * 4096
+    assert lib.splitee_tiled_weights_bytes(N, K) >= N * K * 2
+
+
+def test_tiled_weights_bytes_invalid(lib):
+    assert lib.splitee_tiled_weights_bytes(8, 12) == 0
+    assert lib.splitee_tiled_weights_bytes(-1, 8) == 0
+    assert lib.splitee_tiled_weights_bytes(0, 8) == 0
+
+
+def test_tile_weights_validation(lib):
+    f = lib.splitee_tile_weights
+    big = 1 << 20
+    assert f(P, 8, 4, 12, big, None) == SHAPE    # K % 8
+    assert f(P, 4, 4, 8, big, None) == SHAPE     # ldw < K
+    assert f(None, 8, 4, 8, big, None) == ARG
+    assert f(P, 8, 4, 8, None, None) == ARG
+    assert f(8, 8, 4, 8, big, None) == ALIGN
+    assert f(P, 12, 4, 8, big, None) == ALIGN    # 24-byte row pitch
+    assert f(P, 8, 4, 8, big + 8, None) == ALIGN
+    assert f(big, 8, 4, 8, big + 32, None) == ARG  # Wt overlaps the 64 bytes of W
+    assert f(P, 8, 0, 8, big, None) == OK
+
+
+def test_tiled_weights_are_rejected_where_unsupported(lib):
+    assert lib.splitee_masked_linear(P, PF, 8, P, TILED, 8, P, 8, 2, 8, 8, None) == UNSUP
+    assert lib.splitee_masked_linear(P, PX, 8, 8, TILED, 8, P, 8, 2, 8, 8, None) == ALIGN
+    assert lib.splitee_masked_linear(P, PX, 8, P, TILED, 0, P, 8, 0, 8, 8, None) == OK  # ldw unused
+    assert fused(lib, wt=TILED, prec=PF) == UNSUP
+    assert fused(lib, wt=TILED, W=8) == ALIGN
+    assert fused(lib, wt=TILED, M=0) == OK
+    assert lib.splitee_correction(P, 8, P, TILED, 8, 2, 8, 8, G, 1.0, 1.0, 0, 0, 0, PF, 256, 1 << 20,
+                                  None) == UNSUP
+    assert f64_fused(lib, wt=TILED) == UNSUP
+    assert spectral(lib, wt=TILED)[0] == UNSUP
+
+
+@pytest.mark.parametrize("M,N,K", [(128, 16384, 3072), (128, 5120, 3072), (512, 16384, 3072), (64, 19456, 2560),
+                                   (1, 151936, 2560)])
+def test_workspace_queries_cover_both_layouts(lib, M, N, K):
+    # the largest split-K partial set of either plan fits: tiles x splits x tile floats
+    gq, fq = lib.splitee_gemm_workspace_bytes, lib.splitee_fused_workspace_bytes
+    for prec in (PB, PX):
+        assert fq(M, N, K, prec) >= gq(M, N, K, prec)
+        assert gq(M, N, K, prec) % 4 == 0
