@@ -58,6 +58,10 @@ def parse():
     ap.add_argument("--eps", type=float, default=1.0)
     ap.add_argument("--delta", type=float, default=1.0)
     ap.add_argument("--weight-sets", type=int, default=8)
+    ap.add_argument("--layout", default="auto", choices=["auto", "tiled", "row-major"],
+                    help="bfloat16 weights in the tiled load order (splitee_tile_weights) or row-major; "
+                         "auto: row-major for one or two tokens (the vector-ALU GEMV reads whole rows), "
+                         "tiled otherwise")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -118,7 +122,7 @@ class Path:
     draws the masks of all projection groups, then one launch per projection forms
     fl32(X + eta), multiplies and unmasks."""
 
-    def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets):
+    def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets, layout="auto"):
         self.torch, self.sp = torch, sp
         self.prec, self.mech, self.delta, self.eps = prec, mech, delta, eps
         (self.projs, self.M, self.layers_per_step, nsets, self.w_dtype, bank_rows,
@@ -132,7 +136,10 @@ class Path:
         g = torch.Generator(device=dev)
         g.manual_seed(1)
         wt = sp.SPLITEE_F32 if self.w_dtype == "f32" else sp.SPLITEE_BF16
-        self.wt = wt
+        if layout == "auto":
+            layout = "row-major" if M <= 2 else "tiled"
+        self.tiled = layout == "tiled" and wt == sp.SPLITEE_BF16 and prec != sp.SPLITEE_PREC_F32
+        self.wt = sp.SPLITEE_BF16_TILED if self.tiled else wt
         self.X, self.Xt, self.Y, self.ws = [], [], [], []
         for p in self.projs:
             self.X.append(torch.randn((M, p.K), generator=g, device=dev, dtype=torch.float32))
@@ -152,7 +159,11 @@ class Path:
             Ws, sids = [], []
             for p in self.projs:
                 W = torch.randn((p.N, p.K), generator=g, device=dev) * 0.02
-                Ws.append(W.to(torch.bfloat16) if wt == sp.SPLITEE_BF16 else W)
+                if wt == sp.SPLITEE_BF16:
+                    W = W.to(torch.bfloat16)
+                    if self.tiled:  # stored once in the kernels' load order, like loading a checkpoint
+                        W = sp.tile_weights(W)
+                Ws.append(W)
                 sids.append(WL.stream_id(l, p.group))
             self.W.append(Ws)
             self.sid.append(sids)
@@ -225,7 +236,7 @@ class Path:
 
 def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
     path = Path(torch, sp, WL, name, prec, sp.MECHS[args.mech], args.delta, args.eps,
-                args.weight_sets)
+                args.weight_sets, args.layout)
     nsets = path.nsets
     graphs = None
     if not args.no_graph:
@@ -343,11 +354,11 @@ def gemm_source_sha():
     return h.hexdigest()
 
 
-def measured_traffic(workload, prec_name, names):
+def measured_traffic(workload, prec_name, layout, names):
     """HBM bytes per GEMM + unmask launch from the committed rocprofv3 counter
     summary of this workload (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's
     readings), or None when there is none or the kernel sources changed since."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.md" % (workload, prec_name))
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s_%s.md" % (workload, prec_name, layout))
     if not os.path.exists(path):
         return None
     sha, rows = None, {}
@@ -370,7 +381,7 @@ def counter_launches(torch, sp, WL, args, prec):
     """The GEMM launches alone, for counter collection: after set-up, `n` rounds of
     one launch per projection group (layer 0), in projection order, each followed by
     a device synchronization; these are the run's last dispatches."""
-    path = Path(torch, sp, WL, args.workload, prec, sp.MECHS[args.mech], args.delta, args.eps, 1)
+    path = Path(torch, sp, WL, args.workload, prec, sp.MECHS[args.mech], args.delta, args.eps, 1, args.layout)
     if path.decode:
         path.draw_masks(0)
     else:
@@ -606,7 +617,8 @@ def main():
                     "frac": round(achieved / peak, 4)}
     pname = {v: k for k, v in sp.PRECS.items()}[prec]
     names = [p.name for p in path.projs]
-    traffic = measured_traffic(args.workload, pname, names)
+    layout = "tiled" if path.tiled else "row-major"
+    traffic = measured_traffic(args.workload, pname, layout, names)
     # bf16x3 issues three MFMA passes per algorithmic flop (the exact split of the masked input)
     planes = 3 if prec == sp.SPLITEE_PREC_BF16X3 else 1
     if prec != sp.SPLITEE_PREC_F32 and not path.decode:
@@ -640,7 +652,7 @@ def main():
         "config": {"workload": args.workload, "tokens": path.M, "layers_per_step": path.layers_per_step,
                    "projections": {p.name: [p.K, p.N] for p in path.projs},
                    "mechanism": args.mech, "delta": args.delta, "eps": args.eps,
-                   "precision": pname, "weight_sets": path.nsets, "row0": path.row0,
+                   "precision": pname, "w_layout": layout, "weight_sets": path.nsets, "row0": path.row0,
                    "launch": "eager" if args.no_graph else "hip-graph"},
         "roofline": roofline,
         "correction_ms": round(path.correction_ms, 4),
