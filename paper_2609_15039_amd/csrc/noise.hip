@@ -10,34 +10,34 @@ namespace {
 
 // ------------------------------------------------------------------ kernels
 
-// One thread per pair of elements (half a Philox block), one 8-byte store.
+// One thread per Philox block (four consecutive elements of a row), one 16-byte store.
 __global__ void __launch_bounds__(256) noise_kernel(float* __restrict__ eta, int64_t ld, int64_t M,
                                                     int64_t K, int mech, double scale, uint64_t seed,
                                                     uint64_t sid, uint64_t row0)
 {
-    const int64_t ppr = K >> 1; // pairs per row
-    const int64_t total = M * ppr;
+    const int64_t bpr = K >> 2; // blocks per row
+    const int64_t total = M * bpr;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
          t += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t i = t / ppr, c = t - i * ppr;
-        const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)(K >> 2) + (uint64_t)(c >> 1);
-        float2 v = noise_pair(mech, scale, b, (int)(c & 1), (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
-        *reinterpret_cast<float2*>(eta + i * ld + 2 * c) = v;
+        const int64_t i = t / bpr, c = t - i * bpr;
+        const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)c;
+        *reinterpret_cast<float4*>(eta + i * ld + 4 * c) =
+            noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
     }
 }
 
 // Several noise blocks (same M, row0, mechanism and scale; own K, stream_id and
 // output) in one launch, each repeated `reps` times: repetition r of block q
 // writes at eta[q] + r * rep_stride[q] with stream id sid[q] + r * rep_sid_step.
-// blockIdx.y is the repetition; thread t of it handles pair t of the
-// concatenation of the blocks' M x K / 2 pairs.
+// blockIdx.y is the repetition; thread t of it handles Philox block t of the
+// concatenation of the noise blocks' M x K / 4 Philox blocks.
 struct NoiseBlocks {
     float* eta[splitee::NOISE_MULTI_MAX];
     int64_t ld[splitee::NOISE_MULTI_MAX];
     int64_t K[splitee::NOISE_MULTI_MAX];
     uint64_t sid[splitee::NOISE_MULTI_MAX];
-    int64_t first[splitee::NOISE_MULTI_MAX + 1]; // prefix sums of the blocks' pair counts
+    int64_t first[splitee::NOISE_MULTI_MAX + 1]; // prefix sums of the blocks' Philox block counts
     int64_t rep_stride[splitee::NOISE_MULTI_MAX];
     int count;
     uint64_t rep_sid_step;
@@ -53,70 +53,71 @@ __global__ void __launch_bounds__(256) noise_multi_kernel(NoiseBlocks nb, int me
          t += (int64_t)gridDim.x * blockDim.x) {
         int q = 0;
         while (q + 1 < nb.count && t >= nb.first[q + 1]) ++q;
-        const int64_t K = nb.K[q], ppr = K >> 1, u = t - nb.first[q];
-        const int64_t i = u / ppr, c = u - i * ppr;
-        const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)(K >> 2) + (uint64_t)(c >> 1);
+        const int64_t bpr = nb.K[q] >> 2, u = t - nb.first[q];
+        const int64_t i = u / bpr, c = u - i * bpr;
+        const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)c;
         const uint64_t sid = nb.sid[q] + (uint64_t)r * nb.rep_sid_step;
-        const float2 v = noise_pair(mech, scale, b, (int)(c & 1), (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
-        *reinterpret_cast<float2*>(nb.eta[q] + r * nb.rep_stride[q] + i * nb.ld[q] + 2 * c) = v;
+        *reinterpret_cast<float4*>(nb.eta[q] + r * nb.rep_stride[q] + i * nb.ld[q] + 4 * c) =
+            noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
     }
 }
 
-// Xt = fl32(X + eta) for 2 elements per thread; eta is generated (gen = true) or
-// read; output as float32, one bfloat16 plane, or three bfloat16 planes.  X may
-// be null (X = 0).  Optionally zero-fills `zero_count` words at `zero_ptr` (the
-// split-K tile counters of the GEMM that follows).
+// Xt = fl32(X + eta) for the 4 elements of one Philox block per thread; eta is
+// generated (gen = true) or read; output as float32, one bfloat16 plane, three
+// bfloat16 planes or (F64) the binary64 sum.  X may be null (X = 0).  Optionally
+// zero-fills `zero_count` words at `zero_ptr` (the split-K tile counters of the
+// GEMM that follows).
 template <int PREC, bool GEN>
 __global__ void __launch_bounds__(256) mask_kernel(
     const float* __restrict__ X, int64_t ldx, const float* __restrict__ eta, int64_t ld_eta, int mech,
     double scale, uint64_t seed, uint64_t sid, uint64_t row0, void* __restrict__ Xt, int64_t ldxt,
     int64_t plane_stride, int64_t M, int64_t K, unsigned* __restrict__ zero_ptr, int64_t zero_count)
 {
-    const int64_t ppr = K >> 1;
-    const int64_t total = M * ppr;
+    const int64_t bpr = K >> 2;
+    const int64_t total = M * bpr;
     const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t gstride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t z = gtid; z < zero_count; z += gstride) zero_ptr[z] = 0u;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     for (int64_t t = gtid; t < total; t += gstride) {
-        const int64_t i = t / ppr, c = t - i * ppr;
-        float2 e;
+        const int64_t i = t / bpr, c = t - i * bpr;
+        const float4 x = X ? *reinterpret_cast<const float4*>(X + i * ldx + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 e;
         if (GEN) {
-            const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)(K >> 2) + (uint64_t)(c >> 1);
-            e = noise_pair(mech, scale, b, (int)(c & 1), (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
+            const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)c;
+            e = noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
         } else {
-            e = *reinterpret_cast<const float2*>(eta + i * ld_eta + 2 * c);
+            e = *reinterpret_cast<const float4*>(eta + i * ld_eta + 4 * c);
         }
         if (PREC == SPLITEE_PREC_F64) {
             // one binary64 addition: exact whenever x and eta are within 2^29 of each other in magnitude
-            double2 xd = make_double2((double)e.x, (double)e.y);
+            double2* o = reinterpret_cast<double2*>(reinterpret_cast<double*>(Xt) + i * ldxt + 4 * c);
             if (X) {
-                const float2 x = *reinterpret_cast<const float2*>(X + i * ldx + 2 * c);
-                xd = make_double2((double)x.x + xd.x, (double)x.y + xd.y);
+                o[0] = make_double2((double)x.x + (double)e.x, (double)x.y + (double)e.y);
+                o[1] = make_double2((double)x.z + (double)e.z, (double)x.w + (double)e.w);
+            } else {
+                o[0] = make_double2((double)e.x, (double)e.y);
+                o[1] = make_double2((double)e.z, (double)e.w);
             }
-            *reinterpret_cast<double2*>(reinterpret_cast<double*>(Xt) + i * ldxt + 2 * c) = xd;
             continue;
         }
-        float2 xt;
-        if (X) {
-            const float2 x = *reinterpret_cast<const float2*>(X + i * ldx + 2 * c);
-            xt = make_float2(x.x + e.x, x.y + e.y);
-        } else {
-            xt = e;
-        }
+        const float4 xt = X ? make_float4(x.x + e.x, x.y + e.y, x.z + e.z, x.w + e.w) : e;
         if (PREC == SPLITEE_PREC_F32) {
-            *reinterpret_cast<float2*>(reinterpret_cast<float*>(Xt) + i * ldxt + 2 * c) = xt;
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(Xt) + i * ldxt + 4 * c) = xt;
         } else if (PREC == SPLITEE_PREC_BF16) {
-            *reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(Xt) + i * ldxt + 2 * c) =
-                splitee::bf16_bits_rne(xt.x) | (splitee::bf16_bits_rne(xt.y) << 16);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(Xt) + i * ldxt + 4 * c) =
+                make_uint2(splitee::bf16_bits_rne(xt.x) | (splitee::bf16_bits_rne(xt.y) << 16),
+                           splitee::bf16_bits_rne(xt.z) | (splitee::bf16_bits_rne(xt.w) << 16));
         } else {
-            uint32_t h0, m0, l0, h1, m1, l1;
-            splitee::split3_bf16(xt.x, h0, m0, l0);
-            splitee::split3_bf16(xt.y, h1, m1, l1);
-            uint16_t* base = reinterpret_cast<uint16_t*>(Xt) + i * ldxt + 2 * c;
-            *reinterpret_cast<uint32_t*>(base) = h0 | (h1 << 16);
-            *reinterpret_cast<uint32_t*>(base + plane_stride) = m0 | (m1 << 16);
-            *reinterpret_cast<uint32_t*>(base + 2 * plane_stride) = l0 | (l1 << 16);
+            uint32_t h[4], m[4], l[4];
+            splitee::split3_bf16(xt.x, h[0], m[0], l[0]);
+            splitee::split3_bf16(xt.y, h[1], m[1], l[1]);
+            splitee::split3_bf16(xt.z, h[2], m[2], l[2]);
+            splitee::split3_bf16(xt.w, h[3], m[3], l[3]);
+            uint16_t* base = reinterpret_cast<uint16_t*>(Xt) + i * ldxt + 4 * c;
+            *reinterpret_cast<uint2*>(base) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+            *reinterpret_cast<uint2*>(base + plane_stride) = make_uint2(m[0] | (m[1] << 16), m[2] | (m[3] << 16));
+            *reinterpret_cast<uint2*>(base + 2 * plane_stride) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
         }
     }
 }
@@ -174,7 +175,7 @@ namespace splitee_host {
 int launch_noise(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech, double scale,
                  uint64_t seed, uint64_t sid, uint64_t row0, hipStream_t s)
 {
-    int64_t work = M * (K / 2);
+    int64_t work = M * (K / 4);
     if (work == 0) return SPLITEE_OK;
     hipLaunchKernelGGL(noise_kernel, dim3(grid_for(work, 256)), dim3(256), 0, s, eta, ld_eta, M, K,
                        mech, scale, seed, sid, row0);
@@ -186,7 +187,7 @@ int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, i
                 int64_t ldxt, int64_t plane_stride, int64_t M, int64_t K, unsigned* zero_ptr,
                 int64_t zero_count, hipStream_t s)
 {
-    int64_t work = M * (K / 2);
+    int64_t work = M * (K / 4);
     int64_t items = work > zero_count ? work : zero_count;
     if (items == 0) return SPLITEE_OK;
     dim3 g(grid_for(items, 256)), b(256);
@@ -220,7 +221,7 @@ int launch_noise_multi(float* const* eta, const int64_t* ld, const int64_t* K, c
         nb.K[q] = K[q];
         nb.sid[q] = sid[q];
         nb.rep_stride[q] = rep_stride ? rep_stride[q] : 0;
-        nb.first[q + 1] = nb.first[q] + M * (K[q] / 2);
+        nb.first[q + 1] = nb.first[q] + M * (K[q] / 4);
     }
     nb.rep_sid_step = rep_sid_step;
     const int64_t work = nb.first[count];

@@ -252,25 +252,30 @@ __device__ __forceinline__ void cr_sincos_2pi(uint32_t w, bool force_slow, float
     }
 }
 
-// eta for one pair of consecutive elements of a row: lanes (0,1) or (2,3) of
-// Philox block b (half = 0 or 1).
-__device__ __forceinline__ float2 noise_pair(int mech, double scale, uint64_t b, int half,
-                                             uint32_t sid_lo, uint32_t sid_hi, uint32_t k0, uint32_t k1)
+// eta for the four elements of Philox block b (lanes 0..3): one Philox call, four
+// Laplace transforms or two Box-Muller pairs (words (w0, w1) -> lanes 0, 1 and
+// (w2, w3) -> lanes 2, 3).
+__device__ __forceinline__ float4 noise_block(int mech, double scale, uint64_t b, uint32_t sid_lo, uint32_t sid_hi,
+                                              uint32_t k0, uint32_t k1)
 {
-    if (mech == SPLITEE_MECH_NONE) return make_float2(0.f, 0.f);
-    u32x4 w = philox4x32_10(u32x4{(uint32_t)b, (uint32_t)(b >> 32), sid_lo, sid_hi}, k0, k1);
-    const uint32_t wa = half ? w.z : w.x, wb = half ? w.w : w.y;
-    float2 o;
+    if (mech == SPLITEE_MECH_NONE) return make_float4(0.f, 0.f, 0.f, 0.f);
+    const u32x4 w = philox4x32_10(u32x4{(uint32_t)b, (uint32_t)(b >> 32), sid_lo, sid_hi}, k0, k1);
+    float4 o;
     if (mech == SPLITEE_MECH_LAPLACE) {
-        o.x = (float)(scale * (double)cr_laplace_t(wa, false));
-        o.y = (float)(scale * (double)cr_laplace_t(wb, false));
+        o.x = (float)(scale * (double)cr_laplace_t(w.x, false));
+        o.y = (float)(scale * (double)cr_laplace_t(w.y, false));
+        o.z = (float)(scale * (double)cr_laplace_t(w.z, false));
+        o.w = (float)(scale * (double)cr_laplace_t(w.w, false));
     } else {
-        const float r = cr_gauss_r(wa, false);
-        float sn, cs;
-        cr_sincos_2pi(wb, false, sn, cs);
+        const float r0 = cr_gauss_r(w.x, false), r1 = cr_gauss_r(w.z, false);
+        float s0, c0, s1, c1;
+        cr_sincos_2pi(w.y, false, s0, c0);
+        cr_sincos_2pi(w.w, false, s1, c1);
         // r * c is exact in binary64 (24 + 24 significant bits)
-        o.x = (float)(scale * ((double)r * (double)cs));
-        o.y = (float)(scale * ((double)r * (double)sn));
+        o.x = (float)(scale * ((double)r0 * (double)c0));
+        o.y = (float)(scale * ((double)r0 * (double)s0));
+        o.z = (float)(scale * ((double)r1 * (double)c1));
+        o.w = (float)(scale * ((double)r1 * (double)s1));
     }
     return o;
 }
