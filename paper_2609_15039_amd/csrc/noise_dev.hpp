@@ -204,15 +204,23 @@ __device__ __forceinline__ float round_dd_f32(dd v)
 
 // RN32(r) is the correctly rounded value of the real function whenever the true
 // value lies within |r| 2^-48 of r and no binary32 midpoint lies that close to r.
+// With f = RN32(r) and e = |r| - |f| (exact: the two are within one binary32 ulp),
+// the midpoints next to f lie h_up = ulp(f) / 2 above |f| and h_dn below it, h_dn =
+// ulp(f) / 4 when |f| is a power of two (the spacing halves below it), else ulp(f) / 2;
+// h_up - e and h_dn + e are the distances from |r| to them, exact (Sterbenz) since
+// each midpoint is within a factor 2 of |r|.  Zero, subnormal and non-finite f take
+// the slow path.
 __device__ __forceinline__ bool round_f32_safe(double r, float& out)
 {
-    float f = (float)r;
-    double fd = (double)f;
-    double m_up = 0.5 * (fd + (double)f32_step(f, true));
-    double m_dn = 0.5 * (fd + (double)f32_step(f, false));
-    double d = fmin(fabs(r - m_up), fabs(r - m_dn));
+    const float f = (float)r;
     out = f;
-    return d > fabs(r) * 0x1p-48;
+    const uint32_t fb = __float_as_uint(f) & 0x7FFFFFFFu;
+    const double ar = fabs(r);
+    const double e = ar - (double)__uint_as_float(fb);
+    const double h_up = (double)__uint_as_float(fb & 0x7F800000u) * 0x1p-24;
+    const double h_dn = (fb & 0x007FFFFFu) ? h_up : 0.5 * h_up;
+    const double d = fmin(h_up - e, h_dn + e);
+    return fb >= 0x00800000u && fb < 0x7F800000u && d > ar * 0x1p-48;
 }
 
 // ---------------------------------------------------- the four transforms
