@@ -60,8 +60,8 @@ def parse():
     ap.add_argument("--weight-sets", type=int, default=8)
     ap.add_argument("--layout", default="auto", choices=["auto", "tiled", "row-major"],
                     help="bfloat16 weights in the tiled load order (splitee_tile_weights) or row-major; "
-                         "auto: row-major for one or two tokens (the vector-ALU GEMV reads whole rows), "
-                         "tiled otherwise")
+                         "auto: row-major for one or two tokens of the per-layer projections (the "
+                         "vector-ALU GEMV reads whole rows), tiled otherwise (the LM heads included)")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -137,7 +137,7 @@ class Path:
         g.manual_seed(1)
         wt = sp.SPLITEE_F32 if self.w_dtype == "f32" else sp.SPLITEE_BF16
         if layout == "auto":
-            layout = "row-major" if M <= 2 else "tiled"
+            layout = "row-major" if M <= 2 and "-lmhead-" not in name else "tiled"
         self.tiled = layout == "tiled" and wt == sp.SPLITEE_BF16 and prec != sp.SPLITEE_PREC_F32
         self.wt = sp.SPLITEE_BF16_TILED if self.tiled else wt
         self.X, self.Xt, self.Y, self.ws = [], [], [], []
