@@ -193,3 +193,35 @@ def test_tiled_llama_layer_sampled(M):
 @pytest.mark.parametrize("M", [1, 4, 16, 64, 1024])
 def test_tiled_qwen_layer_sampled(M):
     _sampled_full_size_tiled(WL.QWEN3_4B, M, "bf16x3", sp.SPLITEE_MECH_LAPLACE, O.MECH_LAPLACE, 719.8, 2.0)
+
+
+@pytest.mark.parametrize("M", [128, 4, 64])
+def test_tiled_graph_replay_matches_eager(M):
+    # noise + mask and GEMM + unmask on tiled W captured in a HIP graph: every replay,
+    # with eager work and synchronisations in between, equals the eager result
+    gp = sp.SPLITEE_PREC_BF16X3
+    N, K = 3072, 3072
+    X = dev(WL.gen_x(M, K))
+    T = sp.tile_weights(dev(WL.gen_w(N, K)).to(torch.bfloat16))
+    mech = sp.SPLITEE_MECH_GAUSSIAN
+    C = sp.correction(T, M, mech, 1.0, 1.0, 0, 9, 0, sp.SPLITEE_PREC_BF16X3)
+    Xt = torch.empty((3, M, K), dtype=torch.int16, device=DEV)
+    Y = torch.empty((M, N), device=DEV)
+    ws = sp.workspace(M, N, K, gp, gemm_only=True)
+
+    def step():
+        sp.splitee_noise_mask(X, K, Xt, gp, K, M, K, mech, 1.0, 1.0, 0, 9, 0)
+        sp.splitee_masked_linear_unmask(Xt, gp, K, T, sp.SPLITEE_BF16_TILED, K, C, N, Y, N, M, N, K, ws[0], ws[1])
+
+    step()
+    ref = host(Y).copy()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for r in range(4):
+        Y.fill_(float("nan"))
+        g.replay()
+        got = host(Y)
+        assert np.array_equal(bits(got), bits(ref)), "replay %d" % r
+        step()
+        torch.cuda.synchronize()
