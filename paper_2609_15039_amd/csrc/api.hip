@@ -6,7 +6,7 @@
 
 namespace splitee_host {
 size_t gemm_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);
-size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec);
+size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);
 }
 
 namespace {
@@ -50,7 +50,7 @@ inline bool use_skinny(int64_t M, int prec) { return M <= 16 && prec != SPLITEE_
 
 size_t gemm_ws(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
-    return use_skinny(M, prec) ? splitee_host::skinny_workspace_bytes(M, N, K, prec)
+    return use_skinny(M, prec) ? splitee_host::skinny_workspace_bytes(M, N, K, prec, w_type)
                                : splitee_host::gemm_workspace_bytes(M, N, K, prec, w_type);
 }
 // Workspace queries take no weight layout: the larger of the row-major and the
@@ -63,7 +63,7 @@ size_t gemm_ws_any(int64_t M, int64_t N, int64_t K, int prec)
 }
 size_t gemm_counters(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
-    return use_skinny(M, prec) ? splitee_host::skinny_counter_bytes(M, N, K, prec)
+    return use_skinny(M, prec) ? splitee_host::skinny_counter_bytes(M, N, K, prec, w_type)
                                : splitee_host::gemm_counter_bytes(M, N, K, prec, w_type);
 }
 

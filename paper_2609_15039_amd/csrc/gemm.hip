@@ -1239,6 +1239,164 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
     }
 }
 
+
+// ------------------------------------------------ decode, M <= 2, tiled W
+// A workgroup of 4 waves owns one 32-row block of tiled W and a range of its 64-k
+// tiles.  Lane l of a wave holds row l % 32 and k half l / 32 of every 16-k step, so
+// each W load is the block's contiguous 1 KB step (whole cache lines).  The masked
+// input of the range is formed once into LDS (fl32(X + eta), rounded to bfloat16 for
+// single-pass BF16, or the exact sum of the planes).  Wave w takes the range's tiles
+// w, w + 4, ..; W flows through a ring of GT_RING tiles.  Each lane accumulates
+// fma(x~, w, acc) in k order; the two k halves, the four waves and (K split over
+// workgroups) the splits are then added in that order, so results are deterministic.
+constexpr int GT_RING = 4;
+constexpr int GT_LDS_MAX = 64 * 1024;
+
+template <int NPL, bool MASK, int MR>
+__global__ void __launch_bounds__(GV_WAVES * WAVE)
+gemv_tiled_kernel(SkSrc src, const uint16_t* __restrict__ W, const float* __restrict__ C, int64_t ldc,
+                  float* __restrict__ Out, int64_t ldo, int N, int K, int nblocks, int ksplit, int kt_per_split,
+                  float* __restrict__ part, unsigned* __restrict__ counters)
+{
+    extern __shared__ __attribute__((aligned(16))) float xs[]; // MR rows of 64 kt_per_split floats
+    __shared__ float red[GV_WAVES][MR][32];
+    __shared__ unsigned flag;
+    const int tid = threadIdx.x, lane = tid % WAVE;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int split = (int)lb / nblocks, cb = (int)lb % nblocks;
+    const int ktiles = (K + 63) / 64;
+    const int kt0 = split * kt_per_split, kt1 = min(kt0 + kt_per_split, ktiles);
+    const int nkt = kt1 > kt0 ? kt1 - kt0 : 0;
+    const int XW = 64 * kt_per_split;
+    const int njw = nkt > wave ? (nkt - wave + GV_WAVES - 1) / GV_WAVES : 0; // this wave's tiles
+
+    // 1. the first turn of the W ring (wave-local tile j = range tile wave + 4 j into slot j % GT_RING)
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)((N + 31) / 32) * ktiles * 4096));
+    const uint32_t wbase = (uint32_t)((int64_t)cb * ktiles * 4096 + lane * 16);
+    uint4 ring[GT_RING][4];
+    auto wload = [&](int j, uint4 (&dst)[4]) {
+        const int kt = kt0 + wave + GV_WAVES * j;
+        const bool ok = j < njw;
+#pragma unroll
+        for (int st = 0; st < 4; ++st) dst[st] = load16(rw, ok ? wbase + (uint32_t)(kt * 4 + st) * 1024 : OOB);
+    };
+#pragma unroll
+    for (int u = 0; u < GT_RING; ++u) wload(u, ring[u]);
+
+    // 2. the masked input of the range: unit t = 8 floats of row m at k = 64 kt0 + 8 (t % (XW / 8))
+    {
+        const int upr = XW / 8, units = MR * upr;
+        const int MRr = MR;
+        const __amdgpu_buffer_rsrc_t rx = make_rsrc(MASK ? (const void*)src.X : (const void*)src.A,
+                                                    MASK ? (uint32_t)((int64_t)MRr * src.ldx * 4)
+                                                         : (uint32_t)(((NPL - 1) * src.pstride + (int64_t)MRr * src.lda) * 2));
+        const __amdgpu_buffer_rsrc_t re = make_rsrc(MASK ? (const void*)src.eta : (const void*)src.A,
+                                                    MASK ? (uint32_t)((int64_t)MRr * src.ld_eta * 4) : 0u);
+        for (int t = tid; t < units; t += GV_WAVES * WAVE) {
+            const int m = t / upr, c = t - m * upr, k = 64 * kt0 + 8 * c;
+            const bool ok = k < K;
+            float v[8];
+            if (MASK) {
+                const uint32_t xo = ok ? (uint32_t)(((int64_t)m * src.ldx + k) * 4) : OOB;
+                const uint32_t eo = ok ? (uint32_t)(((int64_t)m * src.ld_eta + k) * 4) : OOB;
+                const uint4 xv[2] = {load16(rx, xo), load16(rx, ok ? xo + 16 : OOB)};
+                const uint4 ev[2] = {load16(re, eo), load16(re, ok ? eo + 16 : OOB)};
+                const float* a = reinterpret_cast<const float*>(xv);
+                const float* e = reinterpret_cast<const float*>(ev);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float x = a[q] + e[q];
+                    if (NPL == 1) x = splitee::bf16_bits_to_f32(splitee::bf16_bits_rne(x));
+                    v[q] = x;
+                }
+            } else {
+                uint4 pl[NPL];
+#pragma unroll
+                for (int p = 0; p < NPL; ++p)
+                    pl[p] = load16(rx, ok ? (uint32_t)((p * src.pstride + (int64_t)m * src.lda + k) * 2) : OOB);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float x = 0.f;
+#pragma unroll
+                    for (int p = 0; p < NPL; ++p) {
+                        const uint32_t wd = reinterpret_cast<const uint32_t*>(&pl[p])[q / 2];
+                        const float t2 = splitee::bf16_bits_to_f32((q & 1) ? (wd >> 16) : (wd & 0xFFFFu));
+                        x = p == 0 ? t2 : x + t2; // hi + mid, then + lo: exact
+                    }
+                    v[q] = x;
+                }
+            }
+            float4* d = reinterpret_cast<float4*>(xs + m * XW + 8 * c);
+            d[0] = make_float4(v[0], v[1], v[2], v[3]);
+            d[1] = make_float4(v[4], v[5], v[6], v[7]);
+        }
+    }
+    __syncthreads();
+
+    // 3. stream W through the ring
+    const int h = lane / 32;
+    float acc[MR];
+#pragma unroll
+    for (int m = 0; m < MR; ++m) acc[m] = 0.f;
+    for (int j0 = 0; j0 < njw; j0 += GT_RING) {
+#pragma unroll
+        for (int u = 0; u < GT_RING; ++u) {
+            const int j = j0 + u;
+            if (j < njw) {
+                const int lt = wave + GV_WAVES * j; // tile within the range
+#pragma unroll
+                for (int st = 0; st < 4; ++st) {
+                    const uint32_t wd[4] = {ring[u][st].x, ring[u][st].y, ring[u][st].z, ring[u][st].w};
+#pragma unroll
+                    for (int m = 0; m < MR; ++m) {
+                        const float4* xp = reinterpret_cast<const float4*>(xs + m * XW + 64 * lt + 16 * st + 8 * h);
+                        const float4 x0 = xp[0], x1 = xp[1];
+                        const float xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const float w = splitee::bf16_bits_to_f32((e & 1) ? (wd[e / 2] >> 16) : (wd[e / 2] & 0xFFFFu));
+                            acc[m] = fmaf(xv[e], w, acc[m]);
+                        }
+                    }
+                }
+            }
+            wload(j + GT_RING, ring[u]);
+        }
+    }
+
+    // 4. lanes l and l + 32 (the two k halves of row l), then the waves in order
+#pragma unroll
+    for (int m = 0; m < MR; ++m) {
+        const float o = __shfl_xor(acc[m], 32);
+        if (lane < 32) red[wave][m][lane] = acc[m] + o;
+    }
+    __syncthreads();
+    const bool owner = tid < MR * 32;
+    const int om = tid / 32, orow = tid % 32, col = 32 * cb + orow;
+    float y = 0.f;
+    if (owner) {
+        y = red[0][om][orow];
+#pragma unroll
+        for (int v = 1; v < GV_WAVES; ++v) y += red[v][om][orow];
+    }
+    if (ksplit == 1) {
+        if (owner && col < N) Out[(int64_t)om * ldo + col] = C ? y - C[(int64_t)om * ldc + col] : y;
+        return;
+    }
+    if (owner) store_partial(&part[(((int64_t)cb * ksplit + split) * MR + om) * 32 + orow], y);
+    if (!splitk_arrive(counters + cb, ksplit, &flag)) return;
+    if (owner) {
+        float sum = 0.f;
+        for (int q = 0; q < ksplit; ++q) {
+            const float v = load_partial(&part[(((int64_t)cb * ksplit + q) * MR + om) * 32 + orow]);
+            sum = q == 0 ? v : sum + v;
+        }
+        if (col < N) Out[(int64_t)om * ldo + col] = C ? sum - C[(int64_t)om * ldc + col] : sum;
+    }
+    if (tid == 0) splitk_reset(counters + cb);
+}
+
 // ------------------------------------------------------------ host planning
 
 struct Plan {
@@ -1366,6 +1524,38 @@ Plan plan_skinny(int64_t M, int64_t N, int64_t K, int prec)
     p.ksplit = p.ktiles > 0 ? (p.ktiles + sps - 1) / sps : 1;
     p.counter_bytes = p.ksplit > 1 ? (((size_t)p.ntiles * 4 + 255) / 256) * 256 : 0;
     p.part_bytes = p.ksplit > 1 ? (size_t)p.ntiles * p.ksplit * 16 * SK_BN * 4 : 0;
+    return p;
+}
+
+// Tiled GEMV (M <= 2, tiled W): the K split (at most 16, at least one 64-k tile per
+// wave, at most about two workgroups per CU) that leaves the busiest CU the fewest
+// tiles when the workgroups are dealt out over 256 CUs (the fewer splits on a tie),
+// then further splits while the masked input of a range exceeds GT_LDS_MAX.
+struct GtPlan {
+    int nblocks, ksplit, kt_per_split;
+    size_t counter_bytes, part_bytes, lds;
+};
+
+GtPlan plan_gemv_tiled(int64_t M, int64_t N, int64_t K)
+{
+    GtPlan p{};
+    p.nblocks = (int)((N + 31) / 32);
+    const int ktiles = (int)((K + 63) / 64);
+    const int ks_max = std::max(1, std::min(std::min(16, ktiles / GV_WAVES), 512 / std::max(p.nblocks, 1)));
+    int ks = 1;
+    int64_t best = -1;
+    for (int c = 1; c <= ks_max; ++c) {
+        const int64_t kps_c = (ktiles + c - 1) / c;
+        const int64_t busiest = ((int64_t)p.nblocks * c + 255) / 256 * kps_c;
+        if (best < 0 || busiest < best) { best = busiest; ks = c; }
+    }
+    int kps = ktiles > 0 ? (ktiles + ks - 1) / ks : 1;
+    while (kps > 1 && (size_t)M * 64 * kps * 4 > (size_t)GT_LDS_MAX) kps = (kps + 1) / 2;
+    p.kt_per_split = std::max(kps, 1);
+    p.ksplit = ktiles > 0 ? (ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
+    p.counter_bytes = p.ksplit > 1 ? (((size_t)p.nblocks * 4 + 255) / 256) * 256 : 0;
+    p.part_bytes = p.ksplit > 1 ? (size_t)p.nblocks * p.ksplit * M * 32 * 4 : 0;
+    p.lds = (size_t)M * 64 * p.kt_per_split * 4;
     return p;
 }
 
@@ -1555,14 +1745,19 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
-size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec)
+size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
+    if (w_type == SPLITEE_BF16_TILED && M <= GV_MMAX) {
+        const GtPlan g = plan_gemv_tiled(M, N, K);
+        return g.counter_bytes + g.part_bytes;
+    }
     Plan p = plan_skinny(M, N, K, prec);
     return p.counter_bytes + p.part_bytes;
 }
 
-size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec)
+size_t skinny_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type)
 {
+    if (w_type == SPLITEE_BF16_TILED && M <= GV_MMAX) return plan_gemv_tiled(M, N, K).counter_bytes;
     return plan_skinny(M, N, K, prec).counter_bytes;
 }
 
@@ -1587,8 +1782,26 @@ int run_skinny(const SkSrc& src, int prec, const void* W, bool tiled, int64_t ld
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
-// M <= 2 runs on the GEMV kernels with row-major W and on the skinny kernel with
-// tiled W (whose loads the GEMV's whole-row reads do not match).
+template <bool MASK>
+int run_gemv_tiled(const SkSrc& src, int prec, const void* W, const float* C, int64_t ldc, float* Out, int64_t ldo,
+                   int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    const GtPlan p = plan_gemv_tiled(M, N, K);
+    if (p.lds > (size_t)GT_LDS_MAX) return SPLITEE_ERR_UNSUPPORTED;
+    if (p.ksplit > 1 && (ws == nullptr || ws_bytes < p.counter_bytes + p.part_bytes)) return SPLITEE_ERR_WORKSPACE;
+    unsigned* counters = p.ksplit > 1 ? reinterpret_cast<unsigned*>(ws) : nullptr;
+    float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
+    const dim3 grid((unsigned)((int64_t)p.nblocks * p.ksplit));
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+#define GT_LAUNCH(NP, MR) hipLaunchKernelGGL((gemv_tiled_kernel<NP, MASK, MR>), grid, dim3(GV_WAVES * WAVE), p.lds, s, src, w, C, ldc, Out, ldo, (int)N, (int)K, p.nblocks, p.ksplit, p.kt_per_split, part, counters)
+    if (prec == SPLITEE_PREC_BF16) { if (M == 1) GT_LAUNCH(1, 1); else GT_LAUNCH(1, 2); }
+    else { if (M == 1) GT_LAUNCH(3, 1); else GT_LAUNCH(3, 2); }
+#undef GT_LAUNCH
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
+}
+
+// M <= 2 runs on the vector-ALU GEMV kernels: whole rows of row-major W, or 32-row
+// blocks of tiled W.
 int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const void* W, int w_type, int64_t ldw,
                   const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M, int64_t N,
                   int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
@@ -1601,7 +1814,9 @@ int launch_skinny(const void* A, int prec, int64_t lda, int64_t pstride, const v
     if ((npl - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31))
         return SPLITEE_ERR_UNSUPPORTED;
     const SkSrc src{reinterpret_cast<const uint16_t*>(A), lda, pstride, nullptr, 0, nullptr, 0};
-    if (M <= GV_MMAX && !tiled) return launch_gemv<false>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
+    if (M <= GV_MMAX)
+        return tiled ? run_gemv_tiled<false>(src, prec, W, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s)
+                     : launch_gemv<false>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
     return run_skinny<false>(src, prec, W, tiled, ldw, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s);
 }
 
@@ -1618,7 +1833,9 @@ int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t 
     if (M * ld_eta * 4 >= (int64_t(1) << 31) || M * ldx * 4 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31))
         return SPLITEE_ERR_UNSUPPORTED;
     const SkSrc src{nullptr, 0, 0, X, ldx, eta, ld_eta};
-    if (M <= GV_MMAX && !tiled) return launch_gemv<true>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
+    if (M <= GV_MMAX)
+        return tiled ? run_gemv_tiled<true>(src, prec, W, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s)
+                     : launch_gemv<true>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
     return run_skinny<true>(src, prec, W, tiled, ldw, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s);
 }
 
