@@ -247,10 +247,10 @@ size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
  * noise arguments are then only validated.  C (M x N, ldc) must be the correction
  * of the same mask, e.g. from splitee_correction with the same noise arguments; for
  * a decode step at positions [t, t+M) pass row0 = t and C = bank + t * ldc.
- * M <= 16 with BF16 or BF16X3 takes the bandwidth-bound decode kernels (M <= 2
- * with row-major W: a vector-ALU GEMV; otherwise the skinny MFMA kernel); given
- * eta_override they form fl32(X + eta) and its bfloat16 planes themselves (one
- * launch, bit-identical to the two-launch path).  Otherwise the tiled
+ * M <= 16 with BF16 or BF16X3 takes the bandwidth-bound decode kernels (M <= 2: a
+ * vector-ALU GEMV, on whole rows of row-major W or 32-row blocks of tiled W; else
+ * the skinny MFMA kernel); given eta_override they form fl32(X + eta) and its
+ * bfloat16 planes themselves (one launch, bit-identical to the two-launch path).  Otherwise the tiled
  * or W-streamed MFMA kernel runs, split over K when the tile count is small.
  * workspace: >= splitee_fused_workspace_bytes(M, N, K, prec) bytes, 256-byte
  * aligned; it must hold zeros before its first use and calls leave it that way.
