@@ -2,7 +2,8 @@
 widest N of the two models (Llama-3.2-3B 3072 -> 128256, Qwen3-4B 2560 -> 151936),
 against the oracle on sampled output columns (the first and last columns of the row,
 which cover the ragged tile at the end, and a random sample).  Bar as for the other
-projections: the Theorem-4 gate per element (see test_gpu_parity.py)."""
+projections: the Theorem-4 gate per element (see test_gpu_parity.py).  Both weight
+layouts: row-major and the tiled order (the launch configuration of the bench)."""
 import numpy as np
 import pytest
 import torch
@@ -25,12 +26,16 @@ def host(t):
     return t.cpu().numpy()
 
 
-@pytest.fixture(scope="module", params=["llama-3.2-3b", "qwen3-4b"])
+@pytest.fixture(scope="module", params=[("llama-3.2-3b", "row-major"), ("llama-3.2-3b", "tiled"),
+                                        ("qwen3-4b", "row-major"), ("qwen3-4b", "tiled")])
 def lm_head(request):
-    model = WL.LLAMA_3B if request.param == "llama-3.2-3b" else WL.QWEN3_4B
+    name, layout = request.param
+    model = WL.LLAMA_3B if name == "llama-3.2-3b" else WL.QWEN3_4B
     proj = model.lm_head()
     W = WL.gen_w(proj.N, proj.K, seed=5)
     Wd = torch.from_numpy(W).to(DEV).to(torch.bfloat16)
+    if layout == "tiled":
+        Wd = sp.tile_weights(Wd)
     yield model, proj, W, Wd
     del Wd
     torch.cuda.empty_cache()
