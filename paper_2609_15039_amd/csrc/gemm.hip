@@ -1417,12 +1417,12 @@ constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 //   M > 128:       128 x 256, 4 waves side by side (variants 10 bf16x3, 12 bf16)
 // With tiled W, 8 waves per workgroup, measured on the same projections and the
 // Qwen3-4B ones at 32, 64 and 1024 tokens:
-//   M <= 64:       64 x 128, 2 x 4 waves, 3 K tiles ahead (variants 26, 27), or
-//                  64 x 256, 8 waves side by side, 2 ahead (variants 24, 25) when N has
-//                  64 or more 256-column tiles
-//   64 < M <= 128: 128 x 128, 2 x 4 waves                (variants 20, 21), or
-//                  128 x 256 when N has 128 or more 128-column tiles (variants 22, 23)
-//   M > 128:       128 x 256, 2 x 4 waves                (variants 22, 23)
+//   M <= 128: 64-row tiles (two M tiles above 64 rows: half the masked-input stage of a
+//             128-row tile, so the 160 KB hold a third K tile in flight): 64 x 128 on
+//             2 x 4 waves, 3 K tiles ahead (variants 26, 27), or 64 x 256 on 8 waves
+//             side by side, 2 ahead (variants 24, 25) when N has 64 or more 256-column
+//             tiles
+//   M > 128:  128 x 256, 2 x 4 waves, 2 ahead (variants 22, 23)
 // The K split fills about 256 CUs, keeps at least ST_MIN_KT K tiles per split and
 // at most ST_MAX_KS splits.
 
@@ -1437,12 +1437,10 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool all
     const bool x3 = prec == SPLITEE_PREC_BF16X3;
     p.bk = 64;
     if (w_type == SPLITEE_BF16_TILED) {
-        if (M <= 64 && (N + 255) / 256 < 64) {
+        if (M <= 128 && (N + 255) / 256 < 64) {
             p.bm = 64; p.bn = 128; p.variant = x3 ? 26 : 27;
-        } else if (M <= 64) {
+        } else if (M <= 128) {
             p.bm = 64; p.bn = 256; p.variant = x3 ? 24 : 25;
-        } else if (M <= 128 && (N + 127) / 128 < 128) {
-            p.bm = 128; p.bn = 128; p.variant = x3 ? 20 : 21;
         } else {
             p.bm = 128; p.bn = 256; p.variant = x3 ? 22 : 23;
         }
@@ -1716,8 +1714,6 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         case 13: ST_LAUNCH(1, 64, 256, 1, 3, 4, false); break;
         case 14: ST_LAUNCH(3, 128, 128, 2, 2, 4, false); break;
         case 15: ST_LAUNCH(1, 128, 128, 2, 2, 4, false); break;
-        case 20: ST_LAUNCH(3, 128, 128, 2, 2, 8, true); break;
-        case 21: ST_LAUNCH(1, 128, 128, 2, 2, 8, true); break;
         case 22: ST_LAUNCH(3, 128, 256, 2, 2, 8, true); break;
         case 23: ST_LAUNCH(1, 128, 256, 2, 2, 8, true); break;
         case 24: ST_LAUNCH(3, 64, 256, 1, 2, 8, true); break;
@@ -1733,7 +1729,6 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
             case 10: case 12: ST_SUM(128, 256, 1, 4); break;
             case 11: case 13: ST_SUM(64, 256, 1, 4); break;
             case 14: case 15: ST_SUM(128, 128, 2, 2); break;
-            case 20: case 21: ST_SUM(128, 128, 2, 4); break;
             case 22: case 23: ST_SUM(128, 256, 2, 4); break;
             case 24: case 25: ST_SUM(64, 256, 1, 8); break;
             default: ST_SUM(64, 128, 2, 4); break;
