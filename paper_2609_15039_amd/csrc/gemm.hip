@@ -1427,7 +1427,9 @@ constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 //             in a fuller last round (Qwen3-4B gate/up at 1024 tokens: 608 tiles, 3
 //             rounds, against 1216 half tiles, 2.5 rounds' work: 361 -> 334 us)
 // The K split fills about 256 CUs, keeps at least ST_MIN_KT K tiles per split and
-// at most ST_MAX_KS splits.
+// at most ST_MAX_KS splits; below that cap it takes the split count with the fewest
+// rounds of 256 workgroups times K tiles per split rounded up to whole turns of the
+// ring (the rest of a turn runs on zero tiles), the fewer splits on a tie.
 
 bool use_stream(int prec, int w_type)
 {
@@ -1461,12 +1463,19 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool all
     p.ntiles = (int)((N + p.bn - 1) / p.bn);
     p.ktiles = (int)((K + p.bk - 1) / p.bk);
     const int tiles = p.mtiles * p.ntiles;
+    // ring stages (K tiles in flight + 1) of the variant
+    const int ring = (p.variant == 11 || p.variant == 13 || p.variant == 26 || p.variant == 27) ? 4 : 3;
     int ks = 1;
     if (allow_split && p.ktiles > 0) {
-        ks = 256 / tiles;
-        if (ks > p.ktiles / ST_MIN_KT) ks = p.ktiles / ST_MIN_KT;
-        if (ks > ST_MAX_KS) ks = ST_MAX_KS;
-        if (ks < 1) ks = 1;
+        int ks_max = 256 / tiles;
+        if (ks_max > p.ktiles / ST_MIN_KT) ks_max = p.ktiles / ST_MIN_KT;
+        if (ks_max > ST_MAX_KS) ks_max = ST_MAX_KS;
+        int64_t best = -1;
+        for (int c = 1; c <= ks_max; ++c) {
+            const int64_t kps = (p.ktiles + c - 1) / c;
+            const int64_t cost = ((int64_t)tiles * c + 255) / 256 * ((kps + ring - 1) / ring * ring);
+            if (best < 0 || cost < best) { best = cost; ks = c; }
+        }
     }
     p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
     p.ksplit = p.ktiles > 0 ? (p.ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
