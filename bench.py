@@ -14,7 +14,9 @@ projection, the 28-layer Llama stack at 512 tokens, the 36-layer Qwen3-4B stack
 at 1024 tokens, and Qwen3-4B decode steps (M tokens at position 1024 of a
 2048-position correction bank).  At decode sizes (M <= 16, bfloat16 modes) a
 layer's masks are drawn by one launch and each projection is one launch that
-forms fl32(X + eta), multiplies and unmasks.
+forms fl32(X + eta), multiplies and unmasks.  The timed steps are captured, in
+order, as one HIP graph and replayed once (after an untimed replay), so the host
+launches once for all of them.
 
 Prints one JSON line.  Fields beyond the common contract: ``roofline`` (the
 GEMM + unmask kernel: each projection group's launches for every layer or
@@ -251,6 +253,13 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
                 path.launches(s)
             graphs.append(gph)
         torch.cuda.synchronize()
+        # the timed steps, in order, as one graph: the host launches once instead of once per
+        # step (a graph launch costs tens of microseconds of host time, more than a small step)
+        timed = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(timed):
+            for s in range(steps):
+                path.launches(s)
+        torch.cuda.synchronize()
 
     def run(s):
         if graphs is not None:
@@ -260,12 +269,19 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
 
     for s in range(warmup):
         run(s)
+    if graphs is not None:
+        timed.replay()  # its first launch uploads the graph: untimed
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(steps):
-        run(s)
+    if graphs is not None:
+        timed.replay()
+    else:
+        for s in range(steps):
+            run(s)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
+    if graphs is not None:
+        del timed
 
     # per-launch duration of the GEMM + unmask kernel of each projection group: its
     # launches for every layer / weight set of the run, back to back in one HIP
@@ -653,7 +669,7 @@ def main():
                    "projections": {p.name: [p.K, p.N] for p in path.projs},
                    "mechanism": args.mech, "delta": args.delta, "eps": args.eps,
                    "precision": pname, "w_layout": layout, "weight_sets": path.nsets, "row0": path.row0,
-                   "launch": "eager" if args.no_graph else "hip-graph"},
+                   "launch": "eager" if args.no_graph else "hip-graph (the timed steps captured as one graph)"},
         "roofline": roofline,
         "correction_ms": round(path.correction_ms, 4),
         "modes": modes,
