@@ -10,21 +10,35 @@ namespace {
 
 // ------------------------------------------------------------------ kernels
 
-// One thread per Philox block (four consecutive elements of a row), one 16-byte store.
+// Launch shape of the noise and mask kernels: blockIdx.y walks the rows, the x
+// dimension the row's units (no 64-bit divide per thread).  A unit is one Philox
+// block (four consecutive elements of a row, 16-byte accesses) or, when the launch
+// has fewer than two waves per SIMD of whole blocks (PAIR), half of one: two lanes
+// then take the two Box-Muller pairs (or Laplace word pairs) of a block, halving the
+// serial chain of binary64 transforms per lane where there are too few waves to
+// hide it.  The values are the same either way.
+constexpr int64_t PAIR_BELOW = 256 * 4 * 64 * 2; // Philox blocks: 256 CUs x 4 SIMDs x 64 lanes x 2 waves
+
+template <bool PAIR>
 __global__ void __launch_bounds__(256) noise_kernel(float* __restrict__ eta, int64_t ld, int64_t M,
                                                     int64_t K, int mech, double scale, uint64_t seed,
                                                     uint64_t sid, uint64_t row0)
 {
-    const int64_t bpr = K >> 2; // blocks per row
-    const int64_t total = M * bpr;
+    constexpr int EPT = PAIR ? 2 : 4; // elements per thread
+    const int64_t bpr = K >> 2;       // Philox blocks per row
+    const int64_t upr = K / EPT;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
-         t += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t i = t / bpr, c = t - i * bpr;
-        const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)c;
-        *reinterpret_cast<float4*>(eta + i * ld + 4 * c) =
-            noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
-    }
+    for (int64_t i = blockIdx.y; i < M; i += gridDim.y)
+        for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < upr;
+             u += (int64_t)gridDim.x * blockDim.x) {
+            const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)(PAIR ? u >> 1 : u);
+            float* o = eta + i * ld + EPT * u;
+            if (PAIR)
+                *reinterpret_cast<float2*>(o) =
+                    noise_half(mech, scale, b, (int)(u & 1), (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
+            else
+                *reinterpret_cast<float4*>(o) = noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
+        }
 }
 
 // Several noise blocks (same M, row0, mechanism and scale; own K, stream_id and
@@ -62,64 +76,88 @@ __global__ void __launch_bounds__(256) noise_multi_kernel(NoiseBlocks nb, int me
     }
 }
 
-// Xt = fl32(X + eta) for the 4 elements of one Philox block per thread; eta is
-// generated (gen = true) or read; output as float32, one bfloat16 plane, three
-// bfloat16 planes or (F64) the binary64 sum.  X may be null (X = 0).  Optionally
-// zero-fills `zero_count` words at `zero_ptr` (the split-K tile counters of the
-// GEMM that follows).
-template <int PREC, bool GEN>
+// Xt = fl32(X + eta) for the elements of one unit (see PAIR_BELOW) per thread; eta
+// is generated (GEN) or read; output as float32, one bfloat16 plane, three bfloat16
+// planes or (F64) the binary64 sum.  X may be null (X = 0).  Optionally zero-fills
+// `zero_count` words at `zero_ptr` (the split-K tile counters of the GEMM that
+// follows).
+template <int PREC, bool GEN, bool PAIR>
 __global__ void __launch_bounds__(256) mask_kernel(
     const float* __restrict__ X, int64_t ldx, const float* __restrict__ eta, int64_t ld_eta, int mech,
     double scale, uint64_t seed, uint64_t sid, uint64_t row0, void* __restrict__ Xt, int64_t ldxt,
     int64_t plane_stride, int64_t M, int64_t K, unsigned* __restrict__ zero_ptr, int64_t zero_count)
 {
+    constexpr int EPT = PAIR ? 2 : 4; // elements per thread
     const int64_t bpr = K >> 2;
-    const int64_t total = M * bpr;
-    const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t gstride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t z = gtid; z < zero_count; z += gstride) zero_ptr[z] = 0u;
+    const int64_t upr = K / EPT;
+    const int64_t flat = ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t fstride = (int64_t)gridDim.x * gridDim.y * blockDim.x;
+    for (int64_t z = flat; z < zero_count; z += fstride) zero_ptr[z] = 0u;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-    for (int64_t t = gtid; t < total; t += gstride) {
-        const int64_t i = t / bpr, c = t - i * bpr;
-        const float4 x = X ? *reinterpret_cast<const float4*>(X + i * ldx + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
-        float4 e;
-        if (GEN) {
-            const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)c;
-            e = noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
-        } else {
-            e = *reinterpret_cast<const float4*>(eta + i * ld_eta + 4 * c);
-        }
-        if (PREC == SPLITEE_PREC_F64) {
-            // one binary64 addition: exact whenever x and eta are within 2^29 of each other in magnitude
-            double2* o = reinterpret_cast<double2*>(reinterpret_cast<double*>(Xt) + i * ldxt + 4 * c);
-            if (X) {
-                o[0] = make_double2((double)x.x + (double)e.x, (double)x.y + (double)e.y);
-                o[1] = make_double2((double)x.z + (double)e.z, (double)x.w + (double)e.w);
+    for (int64_t i = blockIdx.y; i < M; i += gridDim.y)
+        for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < upr;
+             u += (int64_t)gridDim.x * blockDim.x) {
+            const int64_t c = EPT * u; // first element of the unit
+            float x[4] = {0.f, 0.f, 0.f, 0.f}, e[4];
+            if (EPT == 4) {
+                if (X) {
+                    const float4 v = *reinterpret_cast<const float4*>(X + i * ldx + c);
+                    x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+                }
+                float4 v;
+                if (GEN) {
+                    const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)u;
+                    v = noise_block(mech, scale, b, (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
+                } else {
+                    v = *reinterpret_cast<const float4*>(eta + i * ld_eta + c);
+                }
+                e[0] = v.x; e[1] = v.y; e[2] = v.z; e[3] = v.w;
             } else {
-                o[0] = make_double2((double)e.x, (double)e.y);
-                o[1] = make_double2((double)e.z, (double)e.w);
+                if (X) {
+                    const float2 v = *reinterpret_cast<const float2*>(X + i * ldx + c);
+                    x[0] = v.x; x[1] = v.y;
+                }
+                float2 v;
+                if (GEN) {
+                    const uint64_t b = (row0 + (uint64_t)i) * (uint64_t)bpr + (uint64_t)(u >> 1);
+                    v = noise_half(mech, scale, b, (int)(u & 1), (uint32_t)sid, (uint32_t)(sid >> 32), k0, k1);
+                } else {
+                    v = *reinterpret_cast<const float2*>(eta + i * ld_eta + c);
+                }
+                e[0] = v.x; e[1] = v.y; e[2] = 0.f; e[3] = 0.f;
             }
-            continue;
+            if (PREC == SPLITEE_PREC_F64) {
+                // one binary64 addition: exact whenever x and eta are within 2^29 of each other in magnitude
+                double2* o = reinterpret_cast<double2*>(reinterpret_cast<double*>(Xt) + i * ldxt + c);
+                for (int q = 0; q < EPT / 2; ++q)
+                    o[q] = X ? make_double2((double)x[2 * q] + (double)e[2 * q], (double)x[2 * q + 1] + (double)e[2 * q + 1])
+                             : make_double2((double)e[2 * q], (double)e[2 * q + 1]);
+                continue;
+            }
+            float xt[4];
+            for (int q = 0; q < EPT; ++q) xt[q] = X ? x[q] + e[q] : e[q];
+            if (PREC == SPLITEE_PREC_F32) {
+                float* o = reinterpret_cast<float*>(Xt) + i * ldxt + c;
+                if (EPT == 4) *reinterpret_cast<float4*>(o) = make_float4(xt[0], xt[1], xt[2], xt[3]);
+                else *reinterpret_cast<float2*>(o) = make_float2(xt[0], xt[1]);
+                continue;
+            }
+            // bfloat16 planes: plane p of element q in bits p16[p][q]
+            uint32_t p16[3][4];
+            for (int q = 0; q < EPT; ++q) {
+                if (PREC == SPLITEE_PREC_BF16) p16[0][q] = splitee::bf16_bits_rne(xt[q]);
+                else splitee::split3_bf16(xt[q], p16[0][q], p16[1][q], p16[2][q]);
+            }
+            constexpr int NPL = PREC == SPLITEE_PREC_BF16 ? 1 : 3;
+            uint16_t* base = reinterpret_cast<uint16_t*>(Xt) + i * ldxt + c;
+            for (int p = 0; p < NPL; ++p) {
+                if (EPT == 4)
+                    *reinterpret_cast<uint2*>(base + p * plane_stride) =
+                        make_uint2(p16[p][0] | (p16[p][1] << 16), p16[p][2] | (p16[p][3] << 16));
+                else
+                    *reinterpret_cast<uint32_t*>(base + p * plane_stride) = p16[p][0] | (p16[p][1] << 16);
+            }
         }
-        const float4 xt = X ? make_float4(x.x + e.x, x.y + e.y, x.z + e.z, x.w + e.w) : e;
-        if (PREC == SPLITEE_PREC_F32) {
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(Xt) + i * ldxt + 4 * c) = xt;
-        } else if (PREC == SPLITEE_PREC_BF16) {
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(Xt) + i * ldxt + 4 * c) =
-                make_uint2(splitee::bf16_bits_rne(xt.x) | (splitee::bf16_bits_rne(xt.y) << 16),
-                           splitee::bf16_bits_rne(xt.z) | (splitee::bf16_bits_rne(xt.w) << 16));
-        } else {
-            uint32_t h[4], m[4], l[4];
-            splitee::split3_bf16(xt.x, h[0], m[0], l[0]);
-            splitee::split3_bf16(xt.y, h[1], m[1], l[1]);
-            splitee::split3_bf16(xt.z, h[2], m[2], l[2]);
-            splitee::split3_bf16(xt.w, h[3], m[3], l[3]);
-            uint16_t* base = reinterpret_cast<uint16_t*>(Xt) + i * ldxt + 4 * c;
-            *reinterpret_cast<uint2*>(base) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
-            *reinterpret_cast<uint2*>(base + plane_stride) = make_uint2(m[0] | (m[1] << 16), m[2] | (m[3] << 16));
-            *reinterpret_cast<uint2*>(base + 2 * plane_stride) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
-        }
-    }
 }
 
 __global__ void __launch_bounds__(256) unmask_kernel(const float* __restrict__ R, int64_t ldr,
@@ -168,6 +206,16 @@ int grid_for(int64_t work_items, int threads)
     return (int)g;
 }
 
+// Grid of the row-walking kernels: x covers a row's units (at most 4096 workgroups,
+// the kernels stride beyond), y the rows (at most 65535, likewise).
+dim3 row_grid(int64_t M, int64_t units_per_row)
+{
+    int64_t gx = (units_per_row + 255) / 256, gy = M;
+    gx = gx < 1 ? 1 : (gx > 4096 ? 4096 : gx);
+    gy = gy < 1 ? 1 : (gy > 65535 ? 65535 : gy);
+    return dim3((unsigned)gx, (unsigned)gy);
+}
+
 }  // namespace
 
 namespace splitee_host {
@@ -175,10 +223,14 @@ namespace splitee_host {
 int launch_noise(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech, double scale,
                  uint64_t seed, uint64_t sid, uint64_t row0, hipStream_t s)
 {
-    int64_t work = M * (K / 4);
+    const int64_t work = M * (K / 4);
     if (work == 0) return SPLITEE_OK;
-    hipLaunchKernelGGL(noise_kernel, dim3(grid_for(work, 256)), dim3(256), 0, s, eta, ld_eta, M, K,
-                       mech, scale, seed, sid, row0);
+    const bool pair = work < PAIR_BELOW;
+    const dim3 g = row_grid(M, K / (pair ? 2 : 4));
+    if (pair)
+        hipLaunchKernelGGL(noise_kernel<true>, g, dim3(256), 0, s, eta, ld_eta, M, K, mech, scale, seed, sid, row0);
+    else
+        hipLaunchKernelGGL(noise_kernel<false>, g, dim3(256), 0, s, eta, ld_eta, M, K, mech, scale, seed, sid, row0);
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
@@ -187,23 +239,25 @@ int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, i
                 int64_t ldxt, int64_t plane_stride, int64_t M, int64_t K, unsigned* zero_ptr,
                 int64_t zero_count, hipStream_t s)
 {
-    int64_t work = M * (K / 4);
-    int64_t items = work > zero_count ? work : zero_count;
-    if (items == 0) return SPLITEE_OK;
-    dim3 g(grid_for(items, 256)), b(256);
+    const int64_t work = M * (K / 4);
+    if (work == 0 && zero_count == 0) return SPLITEE_OK;
     const bool gen = eta == nullptr;
-#define SPLITEE_MASK_LAUNCH(P, G)                                                                  \
-    hipLaunchKernelGGL((mask_kernel<P, G>), g, b, 0, s, X, ldx, eta, ld_eta, gen_mech, scale, seed, \
+    const bool pair = gen && work < PAIR_BELOW;
+    const dim3 g = row_grid(M, K / (pair ? 2 : 4)), b(256);
+#define SPLITEE_MASK_LAUNCH(P, G, PR)                                                                  \
+    hipLaunchKernelGGL((mask_kernel<P, G, PR>), g, b, 0, s, X, ldx, eta, ld_eta, gen_mech, scale, seed, \
                        sid, row0, Xt, ldxt, plane_stride, M, K, zero_ptr, zero_count)
-    if (prec == SPLITEE_PREC_F32) {
-        if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F32, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F32, false);
-    } else if (prec == SPLITEE_PREC_BF16) {
-        if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16, false);
-    } else if (prec == SPLITEE_PREC_BF16X3) {
-        if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16X3, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_BF16X3, false);
-    } else {
-        if (gen) SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F64, true); else SPLITEE_MASK_LAUNCH(SPLITEE_PREC_F64, false);
-    }
+#define SPLITEE_MASK_PREC(P)                                                                           \
+    do {                                                                                               \
+        if (!gen) SPLITEE_MASK_LAUNCH(P, false, false);                                               \
+        else if (pair) SPLITEE_MASK_LAUNCH(P, true, true);                                            \
+        else SPLITEE_MASK_LAUNCH(P, true, false);                                                     \
+    } while (0)
+    if (prec == SPLITEE_PREC_F32) SPLITEE_MASK_PREC(SPLITEE_PREC_F32);
+    else if (prec == SPLITEE_PREC_BF16) SPLITEE_MASK_PREC(SPLITEE_PREC_BF16);
+    else if (prec == SPLITEE_PREC_BF16X3) SPLITEE_MASK_PREC(SPLITEE_PREC_BF16X3);
+    else SPLITEE_MASK_PREC(SPLITEE_PREC_F64);
+#undef SPLITEE_MASK_PREC
 #undef SPLITEE_MASK_LAUNCH
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }

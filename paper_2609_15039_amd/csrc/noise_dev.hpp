@@ -288,4 +288,28 @@ __device__ __forceinline__ float4 noise_block(int mech, double scale, uint64_t b
     return o;
 }
 
+// Half h (0 or 1) of Philox block b: lanes 2h and 2h + 1 of noise_block, i.e. the
+// Box-Muller pair of words (w_2h, w_2h+1) or their two Laplace transforms.  Two
+// threads that each take one half of a block produce noise_block's values with
+// half of its serial chain of binary64 transforms each.
+__device__ __forceinline__ float2 noise_half(int mech, double scale, uint64_t b, int h, uint32_t sid_lo,
+                                             uint32_t sid_hi, uint32_t k0, uint32_t k1)
+{
+    if (mech == SPLITEE_MECH_NONE) return make_float2(0.f, 0.f);
+    const u32x4 w = philox4x32_10(u32x4{(uint32_t)b, (uint32_t)(b >> 32), sid_lo, sid_hi}, k0, k1);
+    const uint32_t wa = h ? w.z : w.x, wb = h ? w.w : w.y;
+    float2 o;
+    if (mech == SPLITEE_MECH_LAPLACE) {
+        o.x = (float)(scale * (double)cr_laplace_t(wa, false));
+        o.y = (float)(scale * (double)cr_laplace_t(wb, false));
+    } else {
+        const float r = cr_gauss_r(wa, false);
+        float sn, cs;
+        cr_sincos_2pi(wb, false, sn, cs);
+        o.x = (float)(scale * ((double)r * (double)cs));
+        o.y = (float)(scale * ((double)r * (double)sn));
+    }
+    return o;
+}
+
 }  // namespace

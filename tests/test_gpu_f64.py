@@ -34,8 +34,9 @@ def host(t):
 
 @pytest.mark.parametrize("with_x", [True, False])
 @pytest.mark.parametrize("delta", [1.0, DELTA_ACT])
-def test_mask64_bit_exact(with_x, delta):
-    M, K, sid = 37, 264, WL.stream_id(2, 3)
+@pytest.mark.parametrize("M,K", [(37, 264), (130, 4104)])  # half and whole Philox blocks per lane
+def test_mask64_bit_exact(with_x, delta, M, K):
+    sid = WL.stream_id(2, 3)
     X = WL.gen_x(M, K, seed=4)
     Xt = torch.full((M, K + 2), float("nan"), dtype=torch.float64, device=DEV)
     sp.splitee_noise_mask(dev(X) if with_x else None, K, Xt, sp.SPLITEE_PREC_F64, K + 2, M, K, G, delta, 1.0, 5,

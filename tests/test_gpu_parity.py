@@ -60,6 +60,19 @@ def test_noise_bit_exact(mech, delta, eps, seed, sid, row0, M, K, ld):
     assert np.all(np.isnan(got[:, K:]))  # padding columns untouched
 
 
+# Launch shapes of the row-walking noise kernel: below 2^17 Philox blocks a launch
+# gives each lane half a block, above it a whole block; rows past 65535 are walked
+# by the y dimension's stride.  Every shape must give the oracle's bits.
+@pytest.mark.parametrize("mech", ["laplace", "gaussian"])
+@pytest.mark.parametrize("M,K", [(130, 4104), (127, 4104), (65537, 8), (70001, 4)])
+def test_noise_bit_exact_launch_shapes(mech, M, K):
+    g, o = MECH[mech]
+    eta = torch.full((M, K), float("nan"), device=DEV)
+    sp.splitee_noise_gen(eta, K, M, K, g, 3.5, 0.75, 21, 6, 9)
+    ref = O.noise(M, K, o, 3.5, 0.75, 21, 6, 9)
+    assert np.array_equal(bits(host(eta)), bits(ref))
+
+
 def _words(n, seed):
     from tests import pins
     g = np.random.Generator(np.random.PCG64(seed))
@@ -339,6 +352,23 @@ def test_noise_mask_bit_exact(prec, mech):
     X = WL.gen_x(M, K, seed=8)
     got = host(sp.noise_mask(dev(X), gp, g, 825.27, 0.5, 4, 300, 77))
     xt = O.mask(X, O.noise(M, K, o, 825.27, 0.5, 4, 300, 77))
+    if prec == "f32":
+        assert np.array_equal(bits(got[0]), bits(xt))
+    elif prec == "bf16":
+        assert np.array_equal(got[0].view(np.uint16), O.bf16_bits(O.bf16_rne(xt)))
+    else:
+        for p, ref in enumerate(O.split3(xt)):
+            assert np.array_equal(got[p].view(np.uint16), O.bf16_bits(ref))
+
+
+@pytest.mark.parametrize("prec,M,K", [(p, M, K) for p in ("f32", "bf16", "bf16x3") for M, K in ((130, 4104), (65537, 8))]
+                         + [("f32", 70001, 4)])  # bfloat16 rows of 4 elements are not 16-byte aligned
+def test_noise_mask_bit_exact_launch_shapes(prec, M, K):
+    # the generated-noise mask at both lane mappings and past 65535 rows (see above)
+    gp, op = PREC[prec]
+    X = WL.gen_x(M, K, seed=13)
+    got = host(sp.noise_mask(dev(X), gp, sp.SPLITEE_MECH_GAUSSIAN, 2.0, 1.0, 3, 41, 5))
+    xt = O.mask(X, O.noise(M, K, O.MECH_GAUSSIAN, 2.0, 1.0, 3, 41, 5))
     if prec == "f32":
         assert np.array_equal(bits(got[0]), bits(xt))
     elif prec == "bf16":
