@@ -6,10 +6,11 @@
 // transform value is the correctly rounded binary32 value of the real function:
 // it is evaluated in binary64 and kept when the binary64 value is on the right
 // side of every binary32 rounding boundary by more than a relative error budget
-// of 2^-48 (at least 16 binary64 ulps, above the error of the device library's
-// log / sqrt / sincospi), and otherwise recomputed in double-double arithmetic
-// (about 100 correct bits) -- Ziv's strategy.  Included by the noise / mask
-// kernels and by the decode GEMM, which generates its masked-input slice itself.
+// of 2^-48 (at least 16 binary64 ulps, above the error of sqrt and of the log,
+// sin and cos written here for the transforms' arguments), and otherwise
+// recomputed in double-double arithmetic (about 100 correct bits) -- Ziv's
+// strategy.  Included by the noise / mask kernels and by the decode GEMM, which
+// generates its masked-input slice itself.
 #pragma once
 #include "common.hpp"
 #include <math.h>
@@ -223,6 +224,93 @@ __device__ __forceinline__ bool round_f32_safe(double r, float& out)
     return fb >= 0x00800000u && fb < 0x7F800000u && d > ar * 0x1p-48;
 }
 
+// -------------------------------------- binary64 log, sin(pi x), cos(pi x): fast path
+// Written for the arguments the transforms pass: log of a positive normal x with
+// at most 33 significant bits in (2^-34, 1), sin / cos of pi x for x = (2w + 1) 2^-32.
+// Each stays within a few binary64 ulps (relative error about 2^-51), inside the
+// 2^-48 budget of round_f32_safe; the fast and slow paths of every transform are
+// compared on all 2^32 words.
+
+// ln 2 = LN2_HI + LN2_LO to about 2^-98; LN2_HI has 44 significant bits, so e LN2_HI
+// is exact for every binary64 exponent e.
+constexpr double LN2_HI = 0x1.62e42fefa38p-1;
+constexpr double LN2_LO = 0x1.ef35793c7673p-45;
+// pi = PI_HI + PI_LO to about 2^-74; PI_HI has 22 significant bits, so PI_HI r is exact
+// for r = k 2^-32, |k| <= 2^30.
+constexpr double PI_HI = 0x1.921fbp+1;
+constexpr double PI_LO = 0x1.5110b4611a626p-21;
+
+// log x = e ln 2 + log m for x = 2^e m, m in [sqrt(1/2), sqrt(2)); log m = 2 atanh(s),
+// s = (m - 1) / (m + 1), |s| < 0.1716, by the atanh series to s^21 (the first term
+// left out is below 2^-56 of the sum).  m - 1 is exact; s comes from a reciprocal
+// refined by two Newton steps and one correction of the quotient.
+__device__ __forceinline__ double log_fast(double x)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    int e = (int)(b >> 52) - 1023;
+    uint64_t mb = (b & 0x000FFFFFFFFFFFFFull) | 0x3FF0000000000000ull; // m in [1, 2)
+    if (mb >= 0x3FF6A09E667F3BCDull) { mb -= 0x0010000000000000ull; ++e; } // m > sqrt(2): halve
+    const double m = __longlong_as_double((long long)mb);
+    const double f = m - 1.0;
+    const double d = m + 1.0;
+    double y = __builtin_amdgcn_rcp(d);
+    y = fma(fma(-d, y, 1.0), y, y);
+    y = fma(fma(-d, y, 1.0), y, y);
+    double s = f * y;
+    s = fma(fma(-d, s, f), y, s);
+    const double z = s * s;
+    double p = 1.0 / 21.0;
+    p = fma(p, z, 1.0 / 19.0);
+    p = fma(p, z, 1.0 / 17.0);
+    p = fma(p, z, 1.0 / 15.0);
+    p = fma(p, z, 1.0 / 13.0);
+    p = fma(p, z, 1.0 / 11.0);
+    p = fma(p, z, 1.0 / 9.0);
+    p = fma(p, z, 1.0 / 7.0);
+    p = fma(p, z, 1.0 / 5.0);
+    p = fma(p, z, 1.0 / 3.0);
+    const double logm = 2.0 * fma(s * z, p, s); // 2 (s + s^3/3 + ... + s^21/21)
+    const double de = (double)e;
+    return fma(de, LN2_HI, fma(de, LN2_LO, logm));
+}
+
+// sin(pi x) and cos(pi x) for x = (2w + 1) 2^-32 in (0, 2): x = q/2 + r with q the
+// nearest integer to 2x and |r| <= 1/4, both exact in integer arithmetic; then the
+// Taylor polynomials of sin and cos at pi r (|pi r| <= pi/4, the first terms left out
+// below 2^-54 of the value) and the quadrant's swap and signs.
+__device__ __forceinline__ void sincospi_fast(uint32_t w, double& sn, double& cs)
+{
+    const int64_t n = 2 * (int64_t)w + 1;          // x = n 2^-32
+    const int64_t q = (n + (1ll << 30)) >> 31;     // nearest integer to 2x (0..4)
+    const double r = (double)(n - (q << 31)) * 0x1p-32;
+    const double t = fma(PI_LO, r, PI_HI * r);     // pi r
+    const double z = t * t;
+    double ps = 1.0 / 355687428096000.0;           // 1/17!
+    ps = fma(ps, z, -1.0 / 1307674368000.0);       // 1/15!
+    ps = fma(ps, z, 1.0 / 6227020800.0);           // 1/13!
+    ps = fma(ps, z, -1.0 / 39916800.0);            // 1/11!
+    ps = fma(ps, z, 1.0 / 362880.0);               // 1/9!
+    ps = fma(ps, z, -1.0 / 5040.0);                // 1/7!
+    ps = fma(ps, z, 1.0 / 120.0);                  // 1/5!
+    ps = fma(ps, z, -1.0 / 6.0);                   // 1/3!
+    const double sr = fma(t * z, ps, t);           // sin(pi r)
+    double pc = -1.0 / 6402373705728000.0;         // 1/18!
+    pc = fma(pc, z, 1.0 / 20922789888000.0);       // 1/16!
+    pc = fma(pc, z, -1.0 / 87178291200.0);         // 1/14!
+    pc = fma(pc, z, 1.0 / 479001600.0);            // 1/12!
+    pc = fma(pc, z, -1.0 / 3628800.0);             // 1/10!
+    pc = fma(pc, z, 1.0 / 40320.0);                // 1/8!
+    pc = fma(pc, z, -1.0 / 720.0);                 // 1/6!
+    pc = fma(pc, z, 1.0 / 24.0);                   // 1/4!
+    pc = fma(pc, z, -0.5);                         // 1/2!
+    const double cr = fma(z, pc, 1.0);             // cos(pi r)
+    // sin(pi (q/2 + r)), cos(pi (q/2 + r)) by q mod 4
+    const int qq = (int)(q & 3);
+    const double a = (qq & 1) ? cr : sr, c = (qq & 1) ? sr : cr;
+    sn = (qq & 2) ? -a : a;
+    cs = (qq == 1 || qq == 2) ? -c : c;
+}
+
 // ---------------------------------------------------- the four transforms
 
 __device__ __forceinline__ float cr_laplace_t(uint32_t w, bool force_slow)
@@ -232,7 +320,7 @@ __device__ __forceinline__ float cr_laplace_t(uint32_t w, bool force_slow)
     const uint64_t j = upper ? ((1ull << 33) - 2ull * (uint64_t)w - 1ull) : (2ull * (uint64_t)w + 1ull);
     const double x = (double)j * 0x1p-32;
     float f;
-    if (force_slow || !round_f32_safe(log(x), f)) f = round_dd_f32(dd_log(x));
+    if (force_slow || !round_f32_safe(log_fast(x), f)) f = round_dd_f32(dd_log(x));
     return upper ? -f : f;
 }
 
@@ -240,16 +328,15 @@ __device__ __forceinline__ float cr_gauss_r(uint32_t w, bool force_slow)
 {
     const double u = ((double)w + 0.5) * 0x1p-32;
     float f;
-    if (force_slow || !round_f32_safe(sqrt(-2.0 * log(u)), f))
+    if (force_slow || !round_f32_safe(sqrt(-2.0 * log_fast(u)), f))
         f = round_dd_f32(dd_sqrt(dd_mul_d(dd_log(u), -2.0)));
     return f;
 }
 
 __device__ __forceinline__ void cr_sincos_2pi(uint32_t w, bool force_slow, float& sn, float& cs)
 {
-    const double x = (double)(2ull * (uint64_t)w + 1ull) * 0x1p-32; // 2u, exact
     double s64, c64;
-    sincospi(x, &s64, &c64);
+    sincospi_fast(w, s64, c64); // of 2u = (2w + 1) 2^-32
     bool ok_s = !force_slow && round_f32_safe(s64, sn);
     bool ok_c = !force_slow && round_f32_safe(c64, cs);
     if (!(ok_s && ok_c)) {
