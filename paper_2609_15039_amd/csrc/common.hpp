@@ -41,6 +41,27 @@ __device__ __forceinline__ void split3_bf16(float x, uint32_t& hi, uint32_t& mid
     lo = bf16_bits_rne(r2);                // exact: r2 has at most 8 significant bits
 }
 
+// RN bfloat16 bits of a (low half) and b (high half) by the hardware conversion
+// (one v_cvt_pk_bf16_f32: round to nearest even, binary32 denormals kept); the same
+// bits as bf16_bits_rne on every binary32 input, NaNs included (checked on all 2^32).
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_rne(float a, float b)
+{
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// split3_bf16 of a pair: the hi, mid and lo terms of a in the low halves, of b in the
+// high halves.
+__device__ __forceinline__ void split3_bf16x2(float a, float b, uint32_t& hi, uint32_t& mid, uint32_t& lo)
+{
+    hi = bf16x2_rne(a, b);
+    const float ra = a - __uint_as_float(hi << 16), rb = b - __uint_as_float(hi & 0xFFFF0000u);
+    mid = bf16x2_rne(ra, rb);
+    lo = bf16x2_rne(ra - __uint_as_float(mid << 16), rb - __uint_as_float(mid & 0xFFFF0000u));
+}
+
 // Workgroup-id remap so that consecutive logical tiles land on the same XCD.
 // The dispatcher places workgroup b on XCD (b mod 8); tiles that share operands
 // are given consecutive logical ids and thus share that XCD's L2.

@@ -720,15 +720,10 @@ __device__ __forceinline__ void planes_of(const float (&x)[8], uint4 (&q)[NPL])
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
         if (NPL == 1) {
-            reinterpret_cast<uint32_t*>(&q[0])[h] =
-                splitee::bf16_bits_rne(x[2 * h]) | (splitee::bf16_bits_rne(x[2 * h + 1]) << 16);
+            reinterpret_cast<uint32_t*>(&q[0])[h] = splitee::bf16x2_rne(x[2 * h], x[2 * h + 1]);
         } else {
-            uint32_t h0, m0, l0, h1, m1, l1;
-            splitee::split3_bf16(x[2 * h], h0, m0, l0);
-            splitee::split3_bf16(x[2 * h + 1], h1, m1, l1);
-            reinterpret_cast<uint32_t*>(&q[0])[h] = h0 | (h1 << 16);
-            reinterpret_cast<uint32_t*>(&q[1])[h] = m0 | (m1 << 16);
-            reinterpret_cast<uint32_t*>(&q[2])[h] = l0 | (l1 << 16);
+            splitee::split3_bf16x2(x[2 * h], x[2 * h + 1], reinterpret_cast<uint32_t*>(&q[0])[h],
+                                   reinterpret_cast<uint32_t*>(&q[1])[h], reinterpret_cast<uint32_t*>(&q[2])[h]);
         }
     }
 }

@@ -142,20 +142,17 @@ __global__ void __launch_bounds__(256) mask_kernel(
                 else *reinterpret_cast<float2*>(o) = make_float2(xt[0], xt[1]);
                 continue;
             }
-            // bfloat16 planes: plane p of element q in bits p16[p][q]
-            uint32_t p16[3][4];
-            for (int q = 0; q < EPT; ++q) {
-                if (PREC == SPLITEE_PREC_BF16) p16[0][q] = splitee::bf16_bits_rne(xt[q]);
-                else splitee::split3_bf16(xt[q], p16[0][q], p16[1][q], p16[2][q]);
+            // bfloat16 planes: plane p of elements 2j, 2j + 1 packed in pk[p][j]
+            uint32_t pk[3][2];
+            for (int j = 0; j < EPT / 2; ++j) {
+                if (PREC == SPLITEE_PREC_BF16) pk[0][j] = splitee::bf16x2_rne(xt[2 * j], xt[2 * j + 1]);
+                else splitee::split3_bf16x2(xt[2 * j], xt[2 * j + 1], pk[0][j], pk[1][j], pk[2][j]);
             }
             constexpr int NPL = PREC == SPLITEE_PREC_BF16 ? 1 : 3;
             uint16_t* base = reinterpret_cast<uint16_t*>(Xt) + i * ldxt + c;
             for (int p = 0; p < NPL; ++p) {
-                if (EPT == 4)
-                    *reinterpret_cast<uint2*>(base + p * plane_stride) =
-                        make_uint2(p16[p][0] | (p16[p][1] << 16), p16[p][2] | (p16[p][3] << 16));
-                else
-                    *reinterpret_cast<uint32_t*>(base + p * plane_stride) = p16[p][0] | (p16[p][1] << 16);
+                if (EPT == 4) *reinterpret_cast<uint2*>(base + p * plane_stride) = make_uint2(pk[p][0], pk[p][1]);
+                else *reinterpret_cast<uint32_t*>(base + p * plane_stride) = pk[p][0];
             }
         }
 }

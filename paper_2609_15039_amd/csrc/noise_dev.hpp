@@ -6,8 +6,8 @@
 // transform value is the correctly rounded binary32 value of the real function:
 // it is evaluated in binary64 and kept when the binary64 value is on the right
 // side of every binary32 rounding boundary by more than a relative error budget
-// of 2^-48 (at least 16 binary64 ulps, above the error of sqrt and of the log,
-// sin and cos written here for the transforms' arguments), and otherwise
+// of 2^-48 (at least 16 binary64 ulps, above the error of the log, sqrt, sin and
+// cos written here for the transforms' arguments), and otherwise
 // recomputed in double-double arithmetic (about 100 correct bits) -- Ziv's
 // strategy.  Included by the noise / mask kernels and by the decode GEMM, which
 // generates its masked-input slice itself.
@@ -226,7 +226,8 @@ __device__ __forceinline__ bool round_f32_safe(double r, float& out)
 
 // -------------------------------------- binary64 log, sin(pi x), cos(pi x): fast path
 // Written for the arguments the transforms pass: log of a positive normal x with
-// at most 33 significant bits in (2^-34, 1), sin / cos of pi x for x = (2w + 1) 2^-32.
+// at most 33 significant bits in (2^-34, 1), sqrt of -2 log u, sin / cos of pi x for
+// x = (2w + 1) 2^-32.
 // Each stays within a few binary64 ulps (relative error about 2^-51), inside the
 // 2^-48 budget of round_f32_safe; the fast and slow paths of every transform are
 // compared on all 2^32 words.
@@ -272,6 +273,22 @@ __device__ __forceinline__ double log_fast(double x)
     const double logm = 2.0 * fma(s * z, p, s); // 2 (s + s^3/3 + ... + s^21/21)
     const double de = (double)e;
     return fma(de, LN2_HI, fma(de, LN2_LO, logm));
+}
+
+// sqrt v for positive normal v, within about one binary64 ulp: the hardware
+// reciprocal square root refined by two coupled Newton steps on (g, h) ~ (sqrt v,
+// 1 / (2 sqrt v)) and a final correction g + h (v - g^2) (Goldschmidt's method).
+__device__ __forceinline__ double sqrt_fast(double v)
+{
+    const double y = __builtin_amdgcn_rsq(v);
+    double g = v * y, h = 0.5 * y;
+    double r = fma(-g, h, 0.5);
+    g = fma(g, r, g);
+    h = fma(h, r, h);
+    r = fma(-g, h, 0.5);
+    g = fma(g, r, g);
+    h = fma(h, r, h);
+    return fma(fma(-g, g, v), h, g);
 }
 
 // sin(pi x) and cos(pi x) for x = (2w + 1) 2^-32 in (0, 2): x = q/2 + r with q the
@@ -328,7 +345,7 @@ __device__ __forceinline__ float cr_gauss_r(uint32_t w, bool force_slow)
 {
     const double u = ((double)w + 0.5) * 0x1p-32;
     float f;
-    if (force_slow || !round_f32_safe(sqrt(-2.0 * log_fast(u)), f))
+    if (force_slow || !round_f32_safe(sqrt_fast(-2.0 * log_fast(u)), f))
         f = round_dd_f32(dd_sqrt(dd_mul_d(dd_log(u), -2.0)));
     return f;
 }
