@@ -110,7 +110,7 @@ def test_scaled_orthogonal_matrix_gives_its_scale_every_round():
 
 
 def test_rank_one_matrix_converges_after_one_round():
-    # W = a b^T: round 1 gives ||a|| |b . v0| / ||v0||, every later round ||a|| ||b||
+    # W = a b^T: iteration 1 gives ||a|| |b . v0| / ||v0||, every later iteration ||a|| ||b||
     g = np.random.Generator(np.random.PCG64(5))
     a, b = g.standard_normal(300), g.standard_normal(512)
     W = np.outer(a, b).astype(np.float32)
