@@ -62,8 +62,9 @@ def parse():
     ap.add_argument("--weight-sets", type=int, default=8)
     ap.add_argument("--layout", default="auto", choices=["auto", "tiled", "row-major"],
                     help="bfloat16 weights in the tiled load order (splitee_tile_weights) or row-major; "
-                         "auto: row-major for one or two tokens of the per-layer projections (the "
-                         "vector-ALU GEMV reads whole rows), tiled otherwise (the LM heads included)")
+                         "auto: row-major for one or two tokens of projections under 16384 rows (the "
+                         "vector-ALU GEMV reads whole rows), tiled otherwise (gate/up and the LM heads "
+                         "at one or two tokens; 'mixed' when a workload has both)")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -138,10 +139,14 @@ class Path:
         g = torch.Generator(device=dev)
         g.manual_seed(1)
         wt = sp.SPLITEE_F32 if self.w_dtype == "f32" else sp.SPLITEE_BF16
-        if layout == "auto":
-            layout = "row-major" if M <= 2 and "-lmhead-" not in name else "tiled"
-        self.tiled = layout == "tiled" and wt == sp.SPLITEE_BF16 and prec != sp.SPLITEE_PREC_F32
-        self.wt = sp.SPLITEE_BF16_TILED if self.tiled else wt
+        can_tile = wt == sp.SPLITEE_BF16 and prec != sp.SPLITEE_PREC_F32
+        # auto: one or two tokens run the vector-ALU GEMV, which reads whole rows of row-major
+        # W faster for the narrower projections and 32-row blocks of tiled W faster from 16384
+        # rows up (gate/up, the LM heads); every other M runs the MFMA kernels on tiled W
+        self.tiled = [can_tile and (layout == "tiled" or (layout == "auto" and not (M <= 2 and p.N < 16384)))
+                      for p in self.projs]
+        self.wt = [sp.SPLITEE_BF16_TILED if t else wt for t in self.tiled]
+        self.layout = "tiled" if all(self.tiled) else ("row-major" if not any(self.tiled) else "mixed")
         self.X, self.Xt, self.Y, self.ws = [], [], [], []
         for p in self.projs:
             self.X.append(torch.randn((M, p.K), generator=g, device=dev, dtype=torch.float32))
@@ -159,11 +164,11 @@ class Path:
         self.W, self.C, self.sid = [], [], []
         for l in range(nlayers):
             Ws, sids = [], []
-            for p in self.projs:
+            for i, p in enumerate(self.projs):
                 W = torch.randn((p.N, p.K), generator=g, device=dev) * 0.02
                 if wt == sp.SPLITEE_BF16:
                     W = W.to(torch.bfloat16)
-                    if self.tiled:  # stored once in the kernels' load order, like loading a checkpoint
+                    if self.tiled[i]:  # stored once in the kernels' load order, like loading a checkpoint
                         W = sp.tile_weights(W)
                 Ws.append(W)
                 sids.append(WL.stream_id(l, p.group))
@@ -194,11 +199,11 @@ class Path:
         W, C = self.W[l][i], self.C[l][i]
         if self.decode:
             self.sp.splitee_masked_linear_fused(
-                self.X[i], p.K, W, self.wt, p.K, C, C.stride(0), self.Y[i], p.N, M, p.N, p.K, self.mech,
+                self.X[i], p.K, W, self.wt[i], p.K, C, C.stride(0), self.Y[i], p.N, M, p.N, p.K, self.mech,
                 self.delta, self.eps, 0, self.sid[l][i], self.row0, self.eta[i][l % self.layers_per_step], self.prec,
                 self.ws[i][0], self.ws[i][1])
         else:
-            self.sp.splitee_masked_linear_unmask(self.Xt[i], self.prec, p.K, W, self.wt, p.K, C,
+            self.sp.splitee_masked_linear_unmask(self.Xt[i], self.prec, p.K, W, self.wt[i], p.K, C,
                                                  C.stride(0), self.Y[i], p.N, M, p.N, p.K,
                                                  self.ws[i][0], self.ws[i][1])
 
@@ -633,7 +638,7 @@ def main():
                     "frac": round(achieved / peak, 4)}
     pname = {v: k for k, v in sp.PRECS.items()}[prec]
     names = [p.name for p in path.projs]
-    layout = "tiled" if path.tiled else "row-major"
+    layout = path.layout
     traffic = measured_traffic(args.workload, pname, layout, names)
     # bf16x3 issues three MFMA passes per algorithmic flop (the exact split of the masked input)
     planes = 3 if prec == sp.SPLITEE_PREC_BF16X3 else 1
@@ -668,7 +673,9 @@ def main():
         "config": {"workload": args.workload, "tokens": path.M, "layers_per_step": path.layers_per_step,
                    "projections": {p.name: [p.K, p.N] for p in path.projs},
                    "mechanism": args.mech, "delta": args.delta, "eps": args.eps,
-                   "precision": pname, "w_layout": layout, "weight_sets": path.nsets, "row0": path.row0,
+                   "precision": pname, "w_layout": layout,
+                   "w_tiled": [p.name for p, t in zip(path.projs, path.tiled) if t],
+                   "weight_sets": path.nsets, "row0": path.row0,
                    "launch": "eager" if args.no_graph else "hip-graph (the timed steps captured as one graph)"},
         "roofline": roofline,
         "correction_ms": round(path.correction_ms, 4),
