@@ -140,11 +140,7 @@ class Path:
         g.manual_seed(1)
         wt = sp.SPLITEE_F32 if self.w_dtype == "f32" else sp.SPLITEE_BF16
         can_tile = wt == sp.SPLITEE_BF16 and prec != sp.SPLITEE_PREC_F32
-        # auto: one or two tokens run the vector-ALU GEMV, which reads whole rows of row-major
-        # W faster for the narrower projections and 32-row blocks of tiled W faster from 16384
-        # rows up (gate/up, the LM heads); every other M runs the MFMA kernels on tiled W
-        self.tiled = [can_tile and (layout == "tiled" or (layout == "auto" and not (M <= 2 and p.N < 16384)))
-                      for p in self.projs]
+        self.tiled = [can_tile and weight_tiled(layout, M, p.N) for p in self.projs]
         self.wt = [sp.SPLITEE_BF16_TILED if t else wt for t in self.tiled]
         self.layout = "tiled" if all(self.tiled) else ("row-major" if not any(self.tiled) else "mixed")
         self.X, self.Xt, self.Y, self.ws = [], [], [], []
@@ -375,6 +371,16 @@ def gemm_source_sha():
     return h.hexdigest()
 
 
+def weight_tiled(layout, M, N):
+    """Whether a bfloat16 projection of N output rows at M tokens stores W tiled.  auto:
+    one or two tokens run the vector-ALU GEMV, which reads whole rows of row-major W faster
+    for the narrower projections and 32-row blocks of tiled W faster from 16384 rows up
+    (gate/up, the LM heads); every other M runs the MFMA kernels on tiled W."""
+    if layout == "auto":
+        return not (M <= 2 and N < 16384)
+    return layout == "tiled"
+
+
 def measured_traffic(workload, prec_name, layout, names):
     """HBM bytes per GEMM + unmask launch from the committed rocprofv3 counter
     summary of this workload (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy's
@@ -591,7 +597,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the masked linear layer runs on a single MI355X "
-              "(multi-GPU sharding is a design note, not part of this build); use --gpus 1",
+              "(sharding over several GPUs is not implemented); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
     if args.copy_probe_mib:
