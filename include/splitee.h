@@ -274,15 +274,6 @@ int splitee_correction(float* C, int64_t ldc, const void* W, int w_type, int64_t
                        size_t workspace_bytes, void* stream);
 
 /*
- * Test hook: evaluates one correctly rounded noise transform on n words
- * (fn 0: Laplace inverse CDF, 1: sqrt(-2 ln u), 2: cos 2 pi u, 3: sin 2 pi u).
- * force_slow = 1 takes the double-double path for every word instead of only
- * for words whose binary64 value lies near a binary32 rounding boundary.
- */
-int splitee_transform_probe(const uint32_t* words, int64_t n, int fn, int force_slow, float* out,
-                            void* stream);
-
-/*
  * Binary64 variant of the fused call and the correction (SPLITEE_PREC_F64): for a
  * projection whose noise scale is too large for binary32 cancellation, as for the Down
  * projection under Theorem 3 (Sec. "The Case Against the Down Linear Projection": with

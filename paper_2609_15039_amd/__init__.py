@@ -25,7 +25,7 @@ SPLITEE_BOUND_LN, SPLITEE_BOUND_ATT, SPLITEE_BOUND_ACT = 0, 1, 2
 EXPORTED = [
     "splitee_abi_version", "splitee_status_string", "splitee_noise_gen", "splitee_mask",
     "splitee_masked_linear", "splitee_unmask", "splitee_fused_workspace_bytes",
-    "splitee_masked_linear_fused", "splitee_correction", "splitee_transform_probe",
+    "splitee_masked_linear_fused", "splitee_correction",
     "splitee_noise_mask", "splitee_gemm_workspace_bytes", "splitee_masked_linear_unmask",
     "splitee_noise_gen_multi", "splitee_spectral_norm_workspace_bytes", "splitee_spectral_norm",
     "splitee_sensitivity_workspace_bytes", "splitee_sensitivity", "splitee_eps_per_token",
@@ -34,6 +34,8 @@ EXPORTED = [
     "splitee_f64_workspace_bytes", "splitee_masked_linear_fused_f64", "splitee_correction_f64",
     "splitee_tiled_weights_bytes", "splitee_tile_weights",
 ]
+# test hooks (include/splitee_probe.h)
+EXPORTED_PROBE = ["splitee_transform_probe", "splitee_mfma_probe"]
 SPLITEE_PREC_F64 = 3
 SPLITEE_ERR_IO, SPLITEE_ERR_EXHAUSTED, SPLITEE_ERR_FORMAT, SPLITEE_ERR_BUSY = -8, -9, -10, -11
 
@@ -106,6 +108,7 @@ def load():
         "splitee_correction_f64": (I, [P, I64, P, I, I64, I64, I64, I64, I, D, D, U64, U64, U64, P, SZ, P]),
         "splitee_tiled_weights_bytes": (SZ, [I64, I64]),
         "splitee_tile_weights": (I, [P, I64, I64, I64, P, P]),
+        "splitee_mfma_probe": (I, [I, I, P, P, D, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -264,6 +267,11 @@ def splitee_correction(C, ldc, W, w_type, ldw, M, N, K, mech, sensitivity, epsil
 def splitee_transform_probe(words, n, fn, force_slow, out, stream=None):
     _check("splitee_transform_probe", load().splitee_transform_probe(
         _ptr(words), n, fn, force_slow, _ptr(out), _stream(stream)))
+
+
+def splitee_mfma_probe(op, n, a, b, c, d, stream=None):
+    _check("splitee_mfma_probe", load().splitee_mfma_probe(op, n, _ptr(a), _ptr(b), float(c), _ptr(d),
+                                                           _stream(stream)))
 
 
 def splitee_noise_mask(X, ldx, Xt, out_prec, ldxt, M, K, mech, sensitivity, epsilon, seed,

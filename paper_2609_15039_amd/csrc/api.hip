@@ -3,6 +3,7 @@
 #include <math.h>
 
 #include "common.hpp"
+#include "splitee_probe.h"
 
 namespace splitee_host {
 size_t gemm_counter_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);

@@ -15,6 +15,7 @@ import paper_2609_15039_amd as sp
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HDR = os.path.join(ROOT, "include", "splitee.h")
+PROBE_HDR = os.path.join(ROOT, "include", "splitee_probe.h")
 OK, ARG, SHAPE, DTYPE, ALIGN, UNSUP, HIP, WS = 0, -1, -2, -3, -4, -5, -6, -7
 P = 16  # aligned stand-in pointer
 L, G, NONE = 0, 1, 2
@@ -22,8 +23,8 @@ F32, BF16, TILED = 0, 1, 2
 PF, PB, PX = 0, 1, 2
 
 
-def declared_functions():
-    text = open(HDR).read()
+def declared_functions(hdr=HDR):
+    text = open(hdr).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(splitee_\w+)\s*\(", text)))
 
@@ -36,7 +37,9 @@ def lib():
 def test_library_exports_every_declared_function(lib):
     decl = declared_functions()
     assert set(decl) == set(sp.EXPORTED)
-    for name in decl:
+    probe = declared_functions(PROBE_HDR)
+    assert set(probe) == set(sp.EXPORTED_PROBE)
+    for name in decl + probe:
         assert hasattr(lib, name), name
 
 
@@ -149,6 +152,13 @@ def test_workspace_sizes(lib):
     assert q(128, 5120, 3072, PX) >= 3 * 128 * 3072 * 2
     assert q(128, 5120, 3072, PF) >= 128 * 3072 * 4
     assert q(1, 6144, 2560, PX) % 256 == 0
+
+
+def test_mfma_probe_validation(lib):
+    for op, n in ((-1, 1), (4, 1), (0, 0), (0, 65), (3, -2)):
+        assert lib.splitee_mfma_probe(op, n, P, P, 0.0, P, None) == ARG
+    assert lib.splitee_mfma_probe(0, 1, None, P, 0.0, P, None) == ARG
+    assert lib.splitee_mfma_probe(0, 1, P, P, 0.0, None, None) == ARG
 
 
 def test_transform_probe_validation(lib):
