@@ -1,38 +1,44 @@
 #!/usr/bin/env python3
 """Throughput of the DP-masked linear path on one MI355X.
 
-Default workload: one step = the whole hot path for one Llama-3.2-3B-shaped
-layer at a 128-token prefill: for each projection group (QKV 3072->5120,
-O 3072->3072, gate/up 3072->16384, down 8192->3072) noise + mask (one kernel)
-and the GEMM with the fused unmask epilogue (one kernel).  Weights are bf16
-~ N(0, 0.02^2), activations float32 ~ N(0, 1), Gaussian mechanism (Prop. 2)
-with Delta = 1, eps = 1; the corrections eta W^T are precomputed outside the
-timed region (the paper's offline step) and reported separately.  Steps cycle
-through 8 distinct weight sets so the 201 MB per layer is streamed from HBM,
-not the 256 MB MALL.  --workload selects the other shapes: the single float32
-projection, the 28-layer Llama stack at 512 tokens, the 36-layer Qwen3-4B stack
-at 1024 tokens, and Qwen3-4B decode steps (M tokens at position 1024 of a
-2048-position correction bank).  At decode sizes (M <= 16, bfloat16 modes) a
-layer's masks are drawn by one launch and each projection is one launch that
-forms fl32(X + eta), multiplies and unmasks.  The timed steps are captured, in
-order, as one HIP graph and replayed once (after an untimed replay), so the host
-launches once for all of them.
+Default workload: one step = the whole hot path for the 36-layer Qwen3-4B-shaped
+projection stack at a 1024-token prefill: for each layer and projection group (QKV
+2560->6144, O 4096->2560, gate/up 2560->19456, down 9728->2560) noise + mask (one
+kernel) and the GEMM with the fused unmask epilogue (one kernel).  Weights are bf16
+~ N(0, 0.02^2) (random init, stored once in the MFMA kernels' tiled load order),
+activations float32 ~ N(0, 1), Gaussian mechanism (Prop. 2) with Delta = 1, eps = 1
+(the work does not depend on the noise scale); the corrections eta W^T are
+precomputed outside the timed region (the paper's offline step) and reported
+separately.  The timed steps are captured, in order, as one HIP graph and replayed
+once (after an untimed replay), so the host launches once for all of them.
 
-Prints one JSON line.  Fields beyond the common contract: ``roofline`` (the
-GEMM + unmask kernel: each projection group's launches for every layer or
-weight set back to back in one HIP graph, bracketed by HIP events on the stream
-they run on; ``traffic`` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
-summary of the workload when the kernel sources still match it, else null),
-``cpu_baseline`` (the CPU oracle on a bounded sample of the same workload),
-``modes`` (other precision modes), ``correction_ms`` (offline precompute),
-``down_f64`` (the Down projection at Theorem 3's noise scale through the binary64
-path against the bf16x3 one: time and error), ``noise_bank`` (one layer's correction
-banks for 2048 positions: created from the
-GPU corrections into files, then loaded as decode steps and as one batch),
-``noise_scale`` (the offline noise-scale step of the same model: spectral norms
-of W_val, W_up and W_gate by the power method, the sensitivity bounds of
-Theorems 1-3 from them, and the time of one power-method round against the
-HBM roofline of reading W once).
+The same line carries `legs`, the other workloads measured the same way: the
+28-layer Llama-3.2-3B stack at 512 tokens, one Llama layer at 128 tokens (8 weight
+sets cycled so the 201 MB per layer streams from HBM, not the 256 MB MALL), and
+Qwen3-4B decode steps of M = 1, 4, 16, 64 tokens at position 1024 of a 2048-position
+correction bank (per step one launch draws every layer's masks, then each projection
+is one launch that forms fl32(X + eta), multiplies and unmasks).  --workload selects
+another workload as the headline (legs are then skipped), e.g. the single float32
+projection or the LM heads.
+
+Fields beyond the common contract: ``roofline`` -- the dominant launch (the
+projection group with the most flops: gate/up) against the MFMA or HBM peak by its
+algorithmic intensity, each group's launches for every layer back to back in one HIP
+graph, bracketed by HIP events on the stream they run on; ``traffic`` from the
+committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary of the workload when the kernel
+sources still match it, else null; ``step``, the whole step's fraction; ``launches``,
+every group's GEMM launch; the noise + mask launch times and their share of the
+step.  ``cpu_baseline`` (the oracle on a bounded sample of the same workload) and
+``fp_error`` (the analogue of the paper's Table 4: the GPU path's error against the
+oracle per mechanism and eps at the paper's noise scale), both from the one CPU leg
+that runs the oracle; ``modes`` (the other precision modes); ``correction_ms``
+(offline precompute); ``down_f64`` (the Down projection at Theorem 3's noise scale
+through the binary64 path against the bf16x3 one: time and error); ``noise_bank`` (one
+layer's correction banks for 2048 positions: created from the GPU corrections into
+files, then loaded as decode steps and as one batch); ``noise_scale`` (the offline
+noise-scale step of the same model: spectral norms of W_val, W_up, W_gate and W_down
+by the power method, the sensitivity bounds of Theorems 1-3 from them, and the time
+of one power-method round against the HBM roofline of reading W once).
 """
 import argparse
 import json
@@ -54,7 +60,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama3b-layer-m128", choices=WORKLOADS)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=WORKLOADS)
     ap.add_argument("--prec", default="bf16x3", choices=["bf16x3", "bf16", "f32"])
     ap.add_argument("--mech", default="gaussian", choices=["gaussian", "laplace", "none"])
     ap.add_argument("--eps", type=float, default=1.0)
@@ -67,6 +73,8 @@ def parse():
                          "at one or two tokens; 'mixed' when a workload has both)")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="skip the other workloads measured beside the default one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-noise-scale", action="store_true", help="skip the noise-scale leg")
     ap.add_argument("--noise-scale-only", action="store_true", help="run only the noise-scale leg")
@@ -85,6 +93,7 @@ def parse():
     return ap.parse_args()
 
 
+DEFAULT_WORKLOAD = "qwen3-4b-36l-m1024"
 WORKLOADS = ["llama3b-layer-m128", "single-fp32-m32", "llama3b-28l-m512", "qwen3-4b-36l-m1024",
              "qwen3-4b-decode-m1", "qwen3-4b-decode-m4", "qwen3-4b-decode-m16", "qwen3-4b-decode-m64",
              "llama3b-lmhead-m1", "llama3b-lmhead-m15", "llama3b-lmhead-m128",
@@ -210,20 +219,21 @@ class Path:
                                         self.eps, 0, self.row0, reps=self.layers_per_step,
                                         rep_strides=[self.M * K for K in Ks], rep_sid_step=self.sid_step)
 
+    def mask(self, l, i):
+        """Prefill: the noise + mask launch of projection group i of layer (or weight set) l."""
+        p = self.projs[i]
+        self.sp.splitee_noise_mask(self.X[i], p.K, self.Xt[i], self.prec, p.K, self.M, p.K, self.mech,
+                                   self.delta, self.eps, 0, self.sid[l][i], self.row0)
+
     def launches(self, s):
         """All kernels of step s: noise, mask, GEMM and unmask of every projection."""
-        sp, M = self.sp, self.M
         base = (s % self.nsets) * self.layers_per_step
         if self.decode:
             self.draw_masks(base)
         for l in range(base, base + self.layers_per_step):
-            if self.decode:
-                for i in range(len(self.projs)):
-                    self.gemm(l, i)
-                continue
-            for i, p in enumerate(self.projs):
-                sp.splitee_noise_mask(self.X[i], p.K, self.Xt[i], self.prec, p.K, M, p.K, self.mech,
-                                      self.delta, self.eps, 0, self.sid[l][i], self.row0)
+            for i in range(len(self.projs)):
+                if not self.decode:
+                    self.mask(l, i)
                 self.gemm(l, i)
 
     def flops(self):
@@ -284,45 +294,57 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
     if graphs is not None:
         del timed
 
-    # per-launch duration of the GEMM + unmask kernel of each projection group: its
-    # launches for every layer / weight set of the run, back to back in one HIP
-    # graph (eager launches when --no-graph), bracketed by HIP events recorded on
-    # the stream the kernels run on; averaged over launches and repeats
+    # per-launch duration of the GEMM + unmask kernel of each projection group, and of the
+    # noise + mask launch (prefill: per projection group; decode: the one launch per step
+    # that draws every layer's masks): the launches for every layer / weight set of the run,
+    # back to back in one HIP graph (eager launches when --no-graph), bracketed by HIP
+    # events recorded on the stream the kernels run on; averaged over launches and repeats
     nproj = len(path.projs)
-    per_proj_us = [0.0] * nproj
     reps = max(2, min(steps, 20))
-    for i in range(nproj):
-        def gemms(i=i):
-            for s in range(path.nsets):
-                base = s * path.layers_per_step
-                for l in range(base, base + path.layers_per_step):
-                    path.gemm(l, i)
-        n_launch = path.nsets * path.layers_per_step
+    stream = torch.cuda.current_stream()
+
+    def time_launches(fn, n_launch):
         if graphs is not None:
-            gemms()
+            fn()
             torch.cuda.synchronize()
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                gemms()
+                fn()
             go = g.replay
         else:
-            go = gemms
+            go = fn
         go()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
+        e0.record(stream)
         for _ in range(reps):
             go()
-        e1.record()
+        e1.record(stream)
         torch.cuda.synchronize()
-        per_proj_us[i] = e0.elapsed_time(e1) * 1e3 / (reps * n_launch)
-    return path, ms, per_proj_us
+        return e0.elapsed_time(e1) * 1e3 / (reps * n_launch)
+
+    n_layers = path.nsets * path.layers_per_step
+
+    def each_layer(f, i):
+        for l in range(n_layers):
+            f(l, i)
+
+    per_proj_us = [time_launches(lambda i=i: each_layer(path.gemm, i), n_layers) for i in range(nproj)]
+    if path.decode:
+        mask_us = [time_launches(lambda: [path.draw_masks(s * path.layers_per_step) for s in range(path.nsets)],
+                                 path.nsets)]
+    else:
+        mask_us = [time_launches(lambda i=i: each_layer(path.mask, i), n_layers) for i in range(nproj)]
+    return path, ms, per_proj_us, mask_us
 
 
-def cpu_baseline(WL, target_s, projs, tokens, w_dtype):
-    """The oracle (binary128 noise, mask, binary64 GEMM, correction GEMM, unmask) on
-    a row sample of one layer of the same workload; throughput in TFLOP/s of the
-    sample's algorithmic work (2 x rows x N x K per projection group)."""
+def cpu_baseline_leg(torch, sp, WL, target_s, projs, tokens, w_dtype, workload, deltas=None):
+    """The CPU leg, the only part of the bench that runs the oracle (test
+    infrastructure): (1) the oracle (binary128 noise, mask, binary64 GEMM, correction
+    GEMM, unmask) timed on a row sample of one layer of the workload on the host's
+    cores, in TFLOP/s of the sample's algorithmic work (2 x rows x N x K per projection
+    group); (2) the floating-point error of the GPU path against the oracle, the
+    analogue of the paper's Table 4 (see fp_error_table)."""
     import numpy as np
     import oracle as O
     try:
@@ -353,10 +375,87 @@ def cpu_baseline(WL, target_s, projs, tokens, w_dtype):
         total += run(rows)
         reps += 1
     flops = reps * sum(2.0 * rows * p.N * p.K for p in projs)
-    return {"value": flops / total / 1e12, "unit": "TFLOP/s",
+    base = {"value": flops / total / 1e12, "unit": "TFLOP/s",
             "cores": int(max(O.num_threads(), blas_threads)), "kind": "oracle",
             "sample": "%d x %d of %d tokens of one layer's %d projection group(s): noise, mask, GEMM, "
                       "correction GEMM, unmask; %.1f s" % (reps, rows, tokens, len(projs), total)}
+    fp = None
+    if w_dtype == "bf16":
+        del Ws
+        fp = fp_error_table(torch, sp, WL, O, np, projs, tokens, workload, deltas)
+    return base, fp
+
+
+def fp_error_table(torch, sp, WL, O, np, projs, M, workload, deltas=None, nrows=4, ncols=256,
+                   eps_list=(0.5, 2.0, 8.0)):
+    """Table 4 analogue: the fused bf16x3 call of the workload's launch configuration
+    (full M, tiled W) per projection group, mechanism and eps at the paper's noise
+    scale (Theorems 1-3: Delta_LN for QKV and gate/up, Delta_att for O, Delta_act for
+    Down -- from the noise-scale leg when it ran, else the closed forms for alpha = 1,
+    beta = 0 and ||W||_2 ~ 0.02 (sqrt(rows) + sqrt(cols))), against the oracle on
+    nrows x ncols sampled outputs per group: mean |err|, mean Eq. fp-log-bound, their
+    ratio, the share of elements above it, max err / Theorem-4 gate, and mean |err|
+    eps.  QKV, O and gate/up are pooled (the paper's offloaded operators); Down, which
+    the paper keeps in the TEE, is reported on its own."""
+    model = WL.QWEN3_4B if workload.startswith("qwen") else WL.LLAMA_3B
+    d = model.hidden
+    if deltas is None:
+        ln = 2.0 * d ** 0.75
+        sn = lambda r, c: 0.02 * (r ** 0.5 + c ** 0.5)
+        deltas = {"ln": ln, "att": ln * sn(model.kv_dim, d), "act": 2.0 * d * d * sn(model.ff, d) ** 2}
+    dsel = {"qkv": deltas["ln"], "gate_up": deltas["ln"], "o": deltas["att"], "down": deltas["act"]}
+    mechs = {"laplace": (sp.SPLITEE_MECH_LAPLACE, O.MECH_LAPLACE), "gaussian": (sp.SPLITEE_MECH_GAUSSIAN,
+                                                                                 O.MECH_GAUSSIAN)}
+    g = np.random.Generator(np.random.PCG64(5))
+    acc = {}
+    t0 = time.perf_counter()
+    for p in projs:
+        tg = torch.Generator(device="cuda")
+        tg.manual_seed(100 + p.group)
+        Wb = (torch.randn((p.N, p.K), generator=tg, device="cuda") * 0.02).to(torch.bfloat16)
+        W = Wb.float().cpu().numpy()
+        T = sp.tile_weights(Wb)
+        del Wb
+        X = WL.gen_x(M, p.K, seed=1)
+        Xd = torch.from_numpy(X).cuda()
+        rows = g.choice(M, size=min(M, nrows), replace=False)
+        cols = g.choice(p.N, size=min(p.N, ncols), replace=False)
+        Ws = W[cols]
+        ref = O.gemm64(X[rows], Ws)
+        sid = WL.stream_id(0, p.group)
+        for mname, (gm, om) in mechs.items():
+            for eps in eps_list:
+                C = sp.correction(T, M, gm, dsel[p.name], eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
+                Y = sp.masked_linear_fused(Xd, T, C, gm, dsel[p.name], eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
+                Yh = Y[torch.from_numpy(rows).cuda()].cpu().numpy()[:, cols].astype(np.float64)
+                del C, Y
+                e = np.stack([O.noise(1, p.K, om, dsel[p.name], eps, 0, sid, int(i))[0] for i in rows])
+                b = O.error_bounds(X[rows], e, O.mask(X[rows], e), Ws, O.PREC_BF16X3)
+                err = np.abs(Yh - ref)
+                key = (mname, eps, "down" if p.name == "down" else "offloaded")
+                a = acc.setdefault(key, {"err": [], "logb": [], "gate": [], "y": []})
+                a["err"].append(err.ravel())
+                a["logb"].append(b["logb"].ravel())
+                a["gate"].append((err / b["gate"]).ravel())
+                a["y"].append(np.abs(ref).ravel())
+        del T
+        torch.cuda.empty_cache()
+    table = {}
+    for (mname, eps, grp), a in sorted(acc.items()):
+        err, logb = np.concatenate(a["err"]), np.concatenate(a["logb"])
+        y = np.concatenate(a["y"])
+        table.setdefault(grp, {}).setdefault(mname, {})["%g" % eps] = {
+            "mean_err": float("%.4g" % err.mean()), "mean_logb": float("%.4g" % logb.mean()),
+            "logb_over_err": round(float(logb.mean() / err.mean()), 2),
+            "pct_above_logb": round(100.0 * float(np.mean(err > logb)), 3),
+            "max_err_over_gate": float("%.3g" % np.concatenate(a["gate"]).max()),
+            "mean_err_times_eps": float("%.4g" % (err.mean() * eps)),
+            "median_rel_err": float("%.3g" % np.median(err / y))}
+    return {"what": "fused bf16x3 at full size (tiled W) against the oracle on %d x %d sampled outputs per "
+                    "projection group; paper-scale Delta per group; 'offloaded' pools %s" %
+                    (nrows, ncols, ", ".join(p.name for p in projs if p.name != "down")),
+            "delta": {k: float("%.6g" % v) for k, v in dsel.items()}, "model": model.name, "tokens": M,
+            "seconds": round(time.perf_counter() - t0, 1), "table": table}
 
 
 GEMM_SOURCES = ["paper_2609_15039_amd/csrc/gemm.hip", "paper_2609_15039_amd/csrc/common.hpp"]
@@ -592,6 +691,67 @@ def down_f64_leg(torch, sp, WL, workload, M=128, delta=1.66e8, eps=1.0, reps=20)
                          "frac": round(tf / F64_PEAK_TFS, 4)}}
 
 
+def leg_summary(sp, path, ms, per_proj_us, mask_us, prec, workload):
+    """value, ms per step, and the roofline object of one workload: the dominant launch
+    (the projection group with the most algorithmic flops) against the MFMA or HBM peak
+    by its algorithmic intensity, every GEMM launch, the noise + mask launches, and the
+    whole step (algorithmic flops / bytes of the fused minimum over ms per step)."""
+    projs, M, L = path.projs, path.M, path.layers_per_step
+    flops = [2.0 * M * p.N * p.K for p in projs]
+    gb = path.gemm_bytes()
+    planes = 3 if prec == sp.SPLITEE_PREC_BF16X3 else 1
+    f32 = prec == sp.SPLITEE_PREC_F32
+    mfma_peak = FP32_PEAK_TFS if f32 else BF16_PEAK_TFS
+    ridge = mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+    def frac_of(fl, by, us):
+        if fl / by < ridge:
+            a = by / (us * 1e-6) / 1e9
+            return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(a / HBM_PEAK_GBS, 4)}
+        a = fl / (us * 1e-6) / 1e12
+        return {"bound": "mfma", "achieved": round(a, 1), "peak": mfma_peak, "unit": "TFLOP/s",
+                "frac": round(a / mfma_peak, 4)}
+
+    d = max(range(len(projs)), key=lambda i: flops[i])
+    roof = frac_of(flops[d], gb[d], per_proj_us[d])
+    pname = {v: k for k, v in sp.PRECS.items()}[prec]
+    traffic = measured_traffic(workload, pname, path.layout, [p.name for p in projs])
+    roof.update({"kernel": ("%s projection: mask + GEMM + unmask in one launch (masks drawn per step)"
+                            if path.decode else "%s projection: GEMM + unmask launch") % projs[d].name,
+                 "launch_us": round(per_proj_us[d], 2), "algorithmic_bytes": int(gb[d]),
+                 "algorithmic_flops": int(flops[d]), "algorithmic_ai": round(flops[d] / gb[d], 1),
+                 "traffic": None if traffic is None else int(traffic[projs[d].name]),
+                 "traffic_per_launch": traffic and {k: int(v) for k, v in traffic.items()}})
+    if not f32 and not path.decode:
+        issued = planes * flops[d] / (per_proj_us[d] * 1e-6) / 1e12
+        roof.update({"mfma_issued_tflops": round(issued, 1), "mfma_issued_frac": round(issued / BF16_PEAK_TFS, 4),
+                     "mfma_passes": planes})
+    step_flops = L * sum(flops)
+    step_bytes = L * sum(gb)
+    step = frac_of(step_flops, step_bytes, ms * 1e3)
+    mask_total_us = (mask_us[0] if path.decode else L * sum(mask_us))
+    step.update({"what": "whole step: noise, mask, GEMM and unmask of every projection group of %d layer(s); "
+                         "algorithmic flops and fused-minimum bytes over ms per step" % L,
+                 "ms": round(ms, 4), "algorithmic_flops": int(step_flops), "algorithmic_bytes": int(step_bytes),
+                 "noise_mask_us": round(mask_total_us, 1),
+                 "noise_mask_share": round(mask_total_us / (ms * 1e3), 4)})
+    roof["step"] = step
+    roof["launches"] = {p.name: dict(frac_of(flops[i], gb[i], per_proj_us[i]), launch_us=round(per_proj_us[i], 2))
+                        for i, p in enumerate(projs)}
+    roof["noise_mask_launch_us"] = ({"all layers": round(mask_us[0], 2)} if path.decode else
+                                    {p.name: round(u, 2) for p, u in zip(projs, mask_us)})
+    value = step_flops / (ms * 1e-3) / 1e12
+    return {"value": round(value, 3), "ms_per_step": round(ms, 4), "tokens": M, "layers_per_step": L,
+            "projections": {p.name: [p.K, p.N] for p in projs}, "w_layout": path.layout,
+            "w_tiled": [p.name for p, t in zip(projs, path.tiled) if t], "weight_sets": path.nsets,
+            "row0": path.row0}, roof
+
+
+LEGS = ["llama3b-28l-m512", "llama3b-layer-m128", "qwen3-4b-decode-m1", "qwen3-4b-decode-m4",
+        "qwen3-4b-decode-m16", "qwen3-4b-decode-m64"]
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -626,66 +786,49 @@ def main():
         print(json.dumps({"noise_scale": noise_scale_leg(torch, sp, WL, args.workload, args.power_iters)}),
               flush=True)
         return
-    path, ms, per_proj_us = run_mode(torch, sp, WL, args.workload, prec, args, args.steps, args.warmup)
-    flops = path.flops()
-    value = flops / (ms * 1e-3) / 1e12
-    gb = path.gemm_bytes()
-    gemm_us = sum(per_proj_us)
-    gflops = [2.0 * path.M * p.N * p.K for p in path.projs]
-    ai = sum(gflops) / sum(gb)
-    if ai < 315.0 or path.w_dtype == "f32" and ai < 19.7:
-        achieved = sum(gb) / (gemm_us * 1e-6) / 1e9
-        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4)}
-    else:
-        peak = FP32_PEAK_TFS if prec == sp.SPLITEE_PREC_F32 else BF16_PEAK_TFS
-        achieved = sum(gflops) / (gemm_us * 1e-6) / 1e12
-        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                    "frac": round(achieved / peak, 4)}
+    path, ms, per_proj_us, mask_us = run_mode(torch, sp, WL, args.workload, prec, args, args.steps, args.warmup)
+    head, roofline = leg_summary(sp, path, ms, per_proj_us, mask_us, prec, args.workload)
     pname = {v: k for k, v in sp.PRECS.items()}[prec]
-    names = [p.name for p in path.projs]
-    layout = path.layout
-    traffic = measured_traffic(args.workload, pname, layout, names)
-    # bf16x3 issues three MFMA passes per algorithmic flop (the exact split of the masked input)
-    planes = 3 if prec == sp.SPLITEE_PREC_BF16X3 else 1
-    if prec != sp.SPLITEE_PREC_F32 and not path.decode:
-        issued = planes * sum(gflops) / (gemm_us * 1e-6) / 1e12
-        roofline.update({"mfma_issued_tflops": round(issued, 1),
-                         "mfma_issued_frac": round(issued / BF16_PEAK_TFS, 4), "mfma_passes": planes})
-    roofline.update({"traffic": None if traffic is None else int(sum(traffic.values())),
-                     "traffic_per_launch": traffic and {k: int(v) for k, v in traffic.items()},
-                     "kernel": ("mask + GEMM + unmask (one launch per projection group, on the masks "
-                                "one launch per layer draws)") if path.decode
-                               else "GEMM + unmask (one launch per projection group)",
-                     "launch_us": {p.name: round(u, 2) for p, u in zip(path.projs, per_proj_us)},
-                     "bytes_per_launch": {p.name: int(b) for p, b in zip(path.projs, gb)},
-                     "flops_per_launch": {p.name: int(f) for p, f in zip(path.projs, gflops)},
-                     "algorithmic_ai": round(ai, 1)})
+    correction_ms = path.correction_ms
+    projs, M, w_dtype = path.projs, path.M, path.w_dtype
+    del path
+    torch.cuda.empty_cache()
     modes = {}
     if not args.no_modes and args.workload != "single-fp32-m32":
         for mname in ("bf16x3", "bf16", "f32"):
             if sp.PRECS[mname] == prec:
                 continue
-            _, m_ms, m_pp = run_mode(torch, sp, WL, args.workload, sp.PRECS[mname], args,
-                                     max(10, args.steps // 2), 3)
+            mpath, m_ms, m_pp, _ = run_mode(torch, sp, WL, args.workload, sp.PRECS[mname], args,
+                                            max(5, args.steps // 2), 2)
             modes[mname] = {"ms_per_step": round(m_ms, 4),
-                            "tflops": round(flops / (m_ms * 1e-3) / 1e12, 2),
-                            "gemm_us": {p.name: round(u, 2) for p, u in zip(path.projs, m_pp)}}
+                            "tflops": round(mpath.flops() / (m_ms * 1e-3) / 1e12, 2),
+                            "gemm_us": {p.name: round(u, 2) for p, u in zip(mpath.projs, m_pp)}}
+            del mpath
+            torch.cuda.empty_cache()
+    legs = {}
+    if not args.no_legs and args.workload == DEFAULT_WORKLOAD:
+        for name in LEGS:
+            lpath, l_ms, l_pp, l_mask = run_mode(torch, sp, WL, name, prec, args, args.steps, args.warmup)
+            lhead, lroof = leg_summary(sp, lpath, l_ms, l_pp, l_mask, prec, name)
+            lhead["roofline"] = lroof
+            legs[name] = lhead
+            del lpath
+            torch.cuda.empty_cache()
+            print("leg %s: %.3f TFLOP/s, %.4f ms per step" % (name, lhead["value"], lhead["ms_per_step"]),
+                  file=sys.stderr, flush=True)
     out = {
-        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "metric": METRIC, "value": head["value"], "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": pname,
         "data": "synthetic (seeded random activations and random-init weights)",
-        "config": {"workload": args.workload, "tokens": path.M, "layers_per_step": path.layers_per_step,
-                   "projections": {p.name: [p.K, p.N] for p in path.projs},
-                   "mechanism": args.mech, "delta": args.delta, "eps": args.eps,
-                   "precision": pname, "w_layout": layout,
-                   "w_tiled": [p.name for p, t in zip(path.projs, path.tiled) if t],
-                   "weight_sets": path.nsets, "row0": path.row0,
-                   "launch": "eager" if args.no_graph else "hip-graph (the timed steps captured as one graph)"},
+        "config": dict({"workload": args.workload}, **{k: v for k, v in head.items()
+                                                       if k not in ("value", "ms_per_step")},
+                       mechanism=args.mech, delta=args.delta, eps=args.eps, precision=pname,
+                       launch="eager" if args.no_graph else "hip-graph (the timed steps captured as one graph)"),
         "roofline": roofline,
-        "correction_ms": round(path.correction_ms, 4),
+        "correction_ms": round(correction_ms, 4),
         "modes": modes,
+        "legs": legs,
     }
     if not args.no_down_f64:
         out["down_f64"] = down_f64_leg(torch, sp, WL, args.workload)
@@ -694,7 +837,9 @@ def main():
     if not args.no_noise_scale:
         out["noise_scale"] = noise_scale_leg(torch, sp, WL, args.workload, args.power_iters)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(WL, args.cpu_seconds, path.projs, path.M, path.w_dtype)
+        deltas = out["noise_scale"]["delta"] if "noise_scale" in out else None
+        out["cpu_baseline"], out["fp_error"] = cpu_baseline_leg(torch, sp, WL, args.cpu_seconds, projs, M,
+                                                                w_dtype, args.workload, deltas)
     print(json.dumps(out), flush=True)
 
 

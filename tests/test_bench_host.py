@@ -47,3 +47,40 @@ def test_traffic_summary_read_only_while_sources_match(tmp_path, monkeypatch):
     assert bench.measured_traffic("w", "bf16x3", "tiled", names + ["down"]) is None  # a launch missing
     _summary(tmp_path, "stale", [("qkv", 100), ("o", 50)])
     assert bench.measured_traffic("w", "bf16x3", "tiled", names) is None       # kernels changed since
+
+
+class _FakeSp:
+    SPLITEE_PREC_F32, SPLITEE_PREC_BF16, SPLITEE_PREC_BF16X3 = 0, 1, 2
+    PRECS = {"f32": 0, "bf16": 1, "bf16x3": 2}
+
+
+class _FakePath:
+    def __init__(self, M, decode, projs, layers):
+        self.projs, self.M, self.decode, self.layers_per_step = projs, M, decode, layers
+        self.w_dtype, self.layout, self.tiled, self.nsets, self.row0 = "bf16", "tiled", [True] * len(projs), 1, 0
+
+    def gemm_bytes(self):
+        return [2.0 * p.N * p.K + (8.0 if self.decode else 4.0) * self.M * p.K + 8.0 * self.M * p.N
+                for p in self.projs]
+
+
+def test_leg_summary_picks_the_dominant_launch_and_the_whole_step():
+    import workloads as WL
+    projs = WL.QWEN3_4B.projections()
+    path = _FakePath(1024, False, projs, 36)
+    us = [100.0, 80.0, 300.0, 160.0]
+    head, roof = bench.leg_summary(_FakeSp, path, 30.0, us, [20.0, 25.0, 20.0, 60.0], 2, "none")
+    assert roof["kernel"].startswith("gate_up") and roof["bound"] == "mfma"
+    fl = 2.0 * 1024 * 19456 * 2560
+    assert roof["achieved"] == round(fl / 300e-6 / 1e12, 1)
+    assert roof["mfma_issued_frac"] == round(3 * fl / 300e-6 / 1e12 / 2500.0, 4)
+    step_fl = 36 * sum(2.0 * 1024 * p.N * p.K for p in projs)
+    assert roof["step"]["achieved"] == round(step_fl / 30e-3 / 1e12, 1)
+    assert roof["step"]["noise_mask_share"] == round(36 * 125.0 / 30e3, 4)
+    assert head["value"] == round(step_fl / 30e-3 / 1e12, 3)
+    # decode: bandwidth-bound, one mask launch per step
+    dpath = _FakePath(1, True, projs, 36)
+    _, droof = bench.leg_summary(_FakeSp, dpath, 1.8, [9.0, 7.0, 20.0, 13.0], [30.0], 2, "none")
+    assert droof["bound"] == "hbm" and droof["step"]["bound"] == "hbm"
+    assert droof["achieved"] == round(dpath.gemm_bytes()[2] / 20e-6 / 1e9, 1)
+    assert droof["step"]["noise_mask_share"] == round(30.0 / 1800.0, 4)

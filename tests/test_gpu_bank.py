@@ -59,7 +59,7 @@ def test_bank_holds_the_corrections(tmp_path, w_dtype, prec):
     # and the oracle's eta W^T within Higham's bound (3 products per k for the split)
     eta = O.noise(rows, K, O.MECH_GAUSSIAN, delta, eps, 0, sid, row0)
     exact = O.gemm64(eta, W)
-    bound = O.dot_bound(eta, W, k_acc=3 * K if prec == sp.SPLITEE_PREC_BF16X3 else K)
+    bound = O.dot_bound(eta, W, planes=3 if prec == sp.SPLITEE_PREC_BF16X3 else None)
     assert np.all(np.abs(got.astype(np.float64) - exact) <= bound)
 
 

@@ -202,8 +202,8 @@ def test_masked_linear_within_dot_bound(prec, w_dtype, M, N, K):
     xt = O.mask(X, eta)
     A = O.gemm_operand(xt, op)
     err = np.abs(R.astype(np.float64) - O.gemm64(A, W))
-    k_acc = 3 * K if prec == "bf16x3" else K
-    assert np.all(err <= O.dot_bound(A, W, k_acc))
+    planes = {"bf16x3": 3, "bf16": 1}.get(prec)
+    assert np.all(err <= O.dot_bound(A, W, planes=planes))
     # not vacuous: typical error at the float32 level
     assert np.median(err / np.maximum(O.dot_bound(A, W), 1e-30)) < 0.05
 
@@ -218,8 +218,7 @@ def test_correction_within_dot_bound(prec, mech, M, N, K):
     C = host(sp.correction(dev_w(W), M, g, 825.27, 2.0, 3, 77, 10, gp))
     eta = O.noise(M, K, o, 825.27, 2.0, 3, 77, 10)
     err = np.abs(C.astype(np.float64) - O.gemm64(eta, W))
-    k_acc = 3 * K if prec == "bf16x3" else K
-    assert np.all(err <= O.dot_bound(eta, W, k_acc))
+    assert np.all(err <= O.dot_bound(eta, W, planes=3 if prec == "bf16x3" else None))
 
 
 # --------------------------------------------------------------- fused, end to end
@@ -393,8 +392,8 @@ def test_split_k_reduction_matches_single_pass_bound_and_repeats(M, N, K, prec):
     outs = [host(sp.masked_linear_unmask(Xt, gp, Wd, None, ws=ws)) for _ in range(3)]
     assert all(np.array_equal(bits(outs[0]), bits(o)) for o in outs[1:])
     A = O.gemm_operand(O.mask(X, eta), op)
-    k_acc = 3 * K if prec == "bf16x3" else K
-    assert np.all(np.abs(outs[0].astype(np.float64) - O.gemm64(A, W)) <= O.dot_bound(A, W, k_acc))
+    planes = {"bf16x3": 3, "bf16": 1}.get(prec)
+    assert np.all(np.abs(outs[0].astype(np.float64) - O.gemm64(A, W)) <= O.dot_bound(A, W, planes=planes))
 
 
 # ----------------------------------------------------- full-size sampled parity

@@ -72,7 +72,7 @@ def _tiled_case(M, N, K, prec, mech=sp.SPLITEE_MECH_GAUSSIAN, omech=O.MECH_GAUSS
     eta = O.noise(M, K, omech, delta, eps, 0, sid, row0)
     b = O.error_bounds(X, eta, O.mask(X, eta), W, op)
     Cref = O.gemm64(eta, W)
-    return np.abs(Y - O.gemm64(X, W)), b, np.abs(host(C).astype(np.float64) - Cref), O.dot_bound(eta, W, 3 * K)
+    return np.abs(Y - O.gemm64(X, W)), b, np.abs(host(C).astype(np.float64) - Cref), O.dot_bound(eta, W, planes=3)
 
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
@@ -97,7 +97,7 @@ def test_tiled_masked_linear_within_dot_bound(prec, M, N, K):
     R = host(sp.masked_linear(Xt, gp, sp.tile_weights(dev(W).to(torch.bfloat16))))
     A = O.gemm_operand(O.mask(X, eta), op)
     err = np.abs(R.astype(np.float64) - O.gemm64(A, W))
-    assert np.all(err <= O.dot_bound(A, W, 3 * K if prec == "bf16x3" else K))
+    assert np.all(err <= O.dot_bound(A, W, planes=3 if prec == "bf16x3" else 1))
 
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
@@ -157,7 +157,7 @@ def test_tiled_split_k_repeats_and_matches_row_major_bound(M, N, K, prec):
     rowmajor = host(sp.masked_linear_unmask(Xt, gp, Wd, None, ws=ws))
     A = O.gemm_operand(O.mask(X, eta), op)
     ref = O.gemm64(A, W)
-    bound = O.dot_bound(A, W, 3 * K if prec == "bf16x3" else K)
+    bound = O.dot_bound(A, W, planes=3 if prec == "bf16x3" else 1)
     assert np.all(np.abs(outs[0].astype(np.float64) - ref) <= bound)
     assert np.all(np.abs(rowmajor.astype(np.float64) - ref) <= bound)
 

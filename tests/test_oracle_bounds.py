@@ -78,12 +78,27 @@ def test_gate_and_rigorous_term_by_hand():
     b = O.error_bounds(X, eta, Xt, W)
     # precondition S_eta <= (K - 1) S_x: 2.75 <= 9
     assert bool(b["precond"][0, 0])
-    # rigorous term: (1 + u) (gamma_4 (S_t + S_eta) + u (S_x + S_eta)) + u S_x
-    #              = (1 + 2^-24) (5.5 / 4194303 + 5.75 / 2^24) + 3 / 2^24
-    rig = (1 + F(1, 2 ** 24)) * (F(11, 8388606) + F(23, 4 * 2 ** 24)) + F(3, 2 ** 24)
+    u = F(1, 2 ** 24)
+    g4 = F(1, 4194303)
+    # R in binary32 (a fused multiply-add chain): c_R = gamma_4.  C may come from the
+    # bfloat16 matrix cores on three planes: 4 group steps (3 planes x 1 group + 1 extra),
+    # c_C = (gamma_4 + 8 u (1 + gamma_4)) (1 + 2^-6), which exceeds gamma_4 at this tiny K
+    cC = (g4 + 8 * u * (1 + g4)) * F(65, 64)
+    assert F(b["c_R"]) == pytest.approx(g4, rel=1e-15)
+    assert F(b["c_C"]) == pytest.approx(cC, rel=1e-15)
+    # rigorous term: (1 + u) (c_R S_t + c_C S_eta + u (S_x + S_eta)) + u S_x
+    rig = (1 + u) * (g4 * F(11, 4) + cC * F(11, 4) + u * F(23, 4)) + 3 * u
     assert F(float(b["rigor"][0, 0])) == pytest.approx(rig, rel=1e-15)
-    # the gate is Theorem 4 here (17/8388606 + 3/2^24 > the rigorous term)
-    assert b["gate"][0, 0] == b["thm4"][0, 0]
+    # so at K = 4 the gate is the rigorous term, above Theorem 4 (17/8388606 + 3/2^24)
+    assert b["gate"][0, 0] == b["rigor"][0, 0] > b["thm4"][0, 0]
+
+
+def test_gate_is_theorem4_from_moderate_k():
+    # from K = 16 on every kernel's accumulation coefficient is gamma_K, so wherever the
+    # precondition holds the gate is Theorem 4 itself
+    for K in (16, 64, 2560, 9728):
+        assert O.acc_coeff(K, 3) == O.gamma(K) and O.acc_coeff(K, 1) == O.gamma(K)
+    assert O.acc_coeff(8, 3) > O.gamma(8)
 
 
 def test_bf16_terms_by_hand():
