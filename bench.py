@@ -331,8 +331,9 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
 
     per_proj_us = [time_launches(lambda i=i: each_layer(path.gemm, i), n_layers) for i in range(nproj)]
     if path.decode:
-        mask_us = [time_launches(lambda: [path.draw_masks(s * path.layers_per_step) for s in range(path.nsets)],
-                                 path.nsets)]
+        # one launch per step: 16 of them per graph, so that the graph launch itself is amortised
+        mask_us = [time_launches(lambda: [path.draw_masks((s % path.nsets) * path.layers_per_step)
+                                          for s in range(16)], 16)]
     else:
         mask_us = [time_launches(lambda i=i: each_layer(path.mask, i), n_layers) for i in range(nproj)]
     return path, ms, per_proj_us, mask_us
