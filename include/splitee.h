@@ -92,7 +92,8 @@ typedef enum {
     SPLITEE_ERR_IO = -8,
     SPLITEE_ERR_EXHAUSTED = -9,
     SPLITEE_ERR_FORMAT = -10,
-    SPLITEE_ERR_BUSY = -11
+    SPLITEE_ERR_BUSY = -11,
+    SPLITEE_ERR_SCRATCH = -12
 } splitee_status;
 
 typedef enum { SPLITEE_MECH_LAPLACE = 0, SPLITEE_MECH_GAUSSIAN = 1, SPLITEE_MECH_NONE = 2 } splitee_mech;
@@ -261,6 +262,31 @@ int splitee_masked_linear_fused(const float* X, int64_t ldx, const void* W, int 
                                 uint64_t seed, uint64_t stream_id, uint64_t row0,
                                 const float* eta_override, int prec, void* workspace,
                                 size_t workspace_bytes, void* stream);
+
+/*
+ * splitee_masked_linear_fused without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation.  Arguments, results and validation are those of
+ * splitee_masked_linear_fused (the same kernels run, so Y is bit-identical to that
+ * call's); its scratch space (split-K counters and partial tiles, the masked-input
+ * planes) is instead a static device buffer of SPLITEE_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on until the process ends.  The call allocates
+ * nothing: on its first use on a device it looks up that device's copy of the buffer,
+ * and it clears the split-K counters on `stream` itself.
+ *   SPLITEE_ERR_SCRATCH   the shape needs more scratch than the buffer holds (the
+ *                         workspace splitee_fused_workspace_bytes would ask for, roughly
+ *                         M K 6 bytes for BF16X3 plus the split-K partials): use
+ *                         splitee_masked_linear_fused with a caller-owned workspace
+ *   SPLITEE_ERR_HIP       the buffer could not be resolved on the current device
+ * Every call on one GPU uses the same buffer: calls that overlap in time on one GPU
+ * (different streams, or host threads) race and give wrong results; serialise them.
+ */
+#define SPLITEE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int splitee_masked_linear_fused_noalloc(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
+                                        const float* C, int64_t ldc, float* Y, int64_t ldy, int64_t M, int64_t N,
+                                        int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                                        uint64_t stream_id, uint64_t row0, const float* eta_override, int prec,
+                                        void* stream);
 
 /*
  * Correction C = eta W^T (Sec. "Precomputing the Mask and Noise Correction"),

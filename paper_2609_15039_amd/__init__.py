@@ -32,12 +32,14 @@ EXPORTED = [
     "splitee_bank_path", "splitee_bank_workspace_bytes", "splitee_bank_create", "splitee_bank_open",
     "splitee_bank_info", "splitee_bank_load", "splitee_bank_close",
     "splitee_f64_workspace_bytes", "splitee_masked_linear_fused_f64", "splitee_correction_f64",
-    "splitee_tiled_weights_bytes", "splitee_tile_weights",
+    "splitee_tiled_weights_bytes", "splitee_tile_weights", "splitee_masked_linear_fused_noalloc",
 ]
 # test hooks (include/splitee_probe.h)
 EXPORTED_PROBE = ["splitee_transform_probe", "splitee_mfma_probe"]
 SPLITEE_PREC_F64 = 3
 SPLITEE_ERR_IO, SPLITEE_ERR_EXHAUSTED, SPLITEE_ERR_FORMAT, SPLITEE_ERR_BUSY = -8, -9, -10, -11
+SPLITEE_ERR_SCRATCH = -12
+SPLITEE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class BankInfo(ctypes.Structure):
@@ -109,6 +111,8 @@ def load():
         "splitee_tiled_weights_bytes": (SZ, [I64, I64]),
         "splitee_tile_weights": (I, [P, I64, I64, I64, P, P]),
         "splitee_mfma_probe": (I, [I, I, P, P, D, P, P]),
+        "splitee_masked_linear_fused_noalloc": (I, [P, I64, P, I, I64, P, I64, P, I64, I64, I64, I64, I, D, D,
+                                                    U64, U64, U64, P, I, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -255,6 +259,13 @@ def splitee_masked_linear_fused(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K,
         _ptr(X), ldx, _ptr(W), w_type, ldw, _ptr(C), ldc, _ptr(Y), ldy, M, N, K, mech, sensitivity,
         epsilon, seed, stream_id, row0, _ptr(eta_override), prec, _ptr(workspace), workspace_bytes,
         _stream(stream)))
+
+
+def splitee_masked_linear_fused_noalloc(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, mech, sensitivity,
+                                        epsilon, seed, stream_id, row0, eta_override, prec, stream=None):
+    _check("splitee_masked_linear_fused_noalloc", load().splitee_masked_linear_fused_noalloc(
+        _ptr(X), ldx, _ptr(W), w_type, ldw, _ptr(C), ldc, _ptr(Y), ldy, M, N, K, mech, sensitivity, epsilon, seed,
+        stream_id, row0, _ptr(eta_override), prec, _stream(stream)))
 
 
 def splitee_correction(C, ldc, W, w_type, ldw, M, N, K, mech, sensitivity, epsilon, seed,

@@ -2,6 +2,8 @@
 // Semantics of every entry point are documented in include/splitee.h.
 #include <math.h>
 
+#include <mutex>
+
 #include "common.hpp"
 #include "splitee_probe.h"
 
@@ -156,6 +158,38 @@ int check_w_f64(const void* W, int w_type, int64_t ldw, int64_t K)
     return SPLITEE_OK;
 }
 
+// ------------------------------------------------------ no-allocation entry point
+// The scratch space of splitee_masked_linear_fused_noalloc: a file-scope device array
+// (one copy per GPU, held until the process ends).  Host code never passes the
+// array's name to a kernel -- on the host it is only a stand-in symbol -- but the
+// device address hipGetSymbolAddress returns for the current device, looked up once
+// per device and kept.
+static __device__ __align__(256) unsigned char scratch[SPLITEE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex scratch_mutex;
+void* scratch_ptr[SCRATCH_MAX_DEVICES] = {};
+
+// The current device's copy of `scratch`, or nullptr if it cannot be resolved.
+void* scratch_for_current_device()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_MAX_DEVICES) return nullptr;
+    std::lock_guard<std::mutex> lock(scratch_mutex);
+    if (!scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+        scratch_ptr[dev] = p;
+    }
+    return scratch_ptr[dev];
+}
+
+// Zero-fills n words: the split-K tile counters must read zero when a call starts.
+__global__ void __launch_bounds__(256) zero_words_kernel(unsigned* __restrict__ p, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0u;
+}
+
 }  // namespace
 
 extern "C" {
@@ -197,6 +231,9 @@ const char* splitee_status_string(int status)
     case SPLITEE_ERR_EXHAUSTED: return "noise bank has fewer unused rows than requested";
     case SPLITEE_ERR_FORMAT: return "bank file header or size is invalid";
     case SPLITEE_ERR_BUSY: return "bank file is open in another handle";
+    case SPLITEE_ERR_SCRATCH:
+        return "shape needs more scratch than the no-allocation entry point's static device buffer "
+               "(SPLITEE_NOALLOC_SCRATCH_BYTES) holds";
     default: return "unknown status";
     }
 }
@@ -357,6 +394,44 @@ int splitee_masked_linear_fused(const float* X, int64_t ldx, const void* W, int 
     return run_masked(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, mech, sensitivity, epsilon,
                       seed, stream_id, row0, eta_override, prec, workspace, workspace_bytes,
                       as_stream(stream));
+}
+
+int splitee_masked_linear_fused_noalloc(const float* X, int64_t ldx, const void* W, int w_type, int64_t ldw,
+                                        const float* C, int64_t ldc, float* Y, int64_t ldy, int64_t M, int64_t N,
+                                        int64_t K, int mech, double sensitivity, double epsilon, uint64_t seed,
+                                        uint64_t stream_id, uint64_t row0, const float* eta_override, int prec,
+                                        void* stream)
+{
+    // the checks of splitee_masked_linear_fused, then the scratch size against the static buffer
+    int rc = check_noise_args(mech, sensitivity, epsilon);
+    if (rc) return rc;
+    if (!valid_prec(prec)) return SPLITEE_ERR_UNSUPPORTED;
+    if (!dims_ok(M, N, K) || K % 8 != 0 || ldx < K || ldc < N || ldy < N) return SPLITEE_ERR_SHAPE;
+    rc = check_w(W, w_type, ldw, K, prec);
+    if (rc) return rc;
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (!X || !W || !C || !Y) return SPLITEE_ERR_ARG;
+    if (!aligned16(X) || !pitch16(ldx, 4) || !aligned16(C) || !pitch16(ldc, 4) || !aligned16(Y) ||
+        !pitch16(ldy, 4) || (eta_override && !aligned16(eta_override)))
+        return SPLITEE_ERR_ALIGN;
+    const size_t need = align256(gemm_ws(M, N, K, prec, w_type)) +
+                        align256((size_t)(prec_planes(prec) * M * K * prec_elsize(prec)));
+    if (need > (size_t)SPLITEE_NOALLOC_SCRATCH_BYTES) return SPLITEE_ERR_SCRATCH;
+    void* ws = scratch_for_current_device();
+    if (!ws) return SPLITEE_ERR_HIP;
+    hipStream_t s = as_stream(stream);
+    // the previous call on this device left the counters zeroed; clear them anyway, so that
+    // the call does not depend on that (the mask kernel of the two-launch path clears them
+    // too, the decode path with a precomputed mask has no such launch)
+    const int64_t nc = (int64_t)(gemm_counters(M, N, K, prec, w_type) / 4);
+    if (nc > 0) {
+        const int64_t blocks = (nc + 255) / 256 < 1024 ? (nc + 255) / 256 : 1024;
+        hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                           reinterpret_cast<unsigned*>(ws), nc);
+        if (hipGetLastError() != hipSuccess) return SPLITEE_ERR_HIP;
+    }
+    return run_masked(X, ldx, W, w_type, ldw, C, ldc, Y, ldy, M, N, K, mech, sensitivity, epsilon, seed, stream_id,
+                      row0, eta_override, prec, ws, (size_t)SPLITEE_NOALLOC_SCRATCH_BYTES, s);
 }
 
 int splitee_correction(float* C, int64_t ldc, const void* W, int w_type, int64_t ldw, int64_t M,

@@ -309,3 +309,24 @@ def test_workspace_queries_cover_both_layouts(lib, M, N, K):
     for prec in (PB, PX):
         assert fq(M, N, K, prec) >= gq(M, N, K, prec)
         assert gq(M, N, K, prec) % 4 == 0
+
+
+def test_noalloc_validation(lib):
+    # the fused call's checks, then the static scratch limit, all before any device call
+    G3 = PX
+    fn = lib.splitee_masked_linear_fused_noalloc
+    args = dict(X=P, ldx=264, W=P, wt=BF16, ldw=264, C=P, ldc=96, Y=P, ldy=96, M=37, N=96, K=264, mech=G, d=1.0,
+                e=1.0, eta=None, prec=G3)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return fn(a["X"], a["ldx"], a["W"], a["wt"], a["ldw"], a["C"], a["ldc"], a["Y"], a["ldy"], a["M"], a["N"],
+                  a["K"], a["mech"], a["d"], a["e"], 0, 0, 0, a["eta"], a["prec"], None)
+
+    assert call(e=0.0) == ARG
+    assert call(K=260, ldx=264, ldw=264) == SHAPE
+    assert call(X=8) == ALIGN
+    assert call(X=None) == ARG
+    assert call(prec=7) == UNSUP
+    assert call(M=0) == OK
+    assert call(M=4096, N=2560, K=9728, ldx=9728, ldw=9728, ldc=2560, ldy=2560) == sp.SPLITEE_ERR_SCRATCH
