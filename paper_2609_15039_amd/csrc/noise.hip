@@ -203,11 +203,21 @@ int grid_for(int64_t work_items, int threads)
     return (int)g;
 }
 
+// Workgroup width of the row-walking kernels: the widest of 256, 128 and 64 threads
+// that divides a row's units, so that no thread of a row's last workgroup idles (a
+// row of 640 units -- K = 2560 -- takes five 128-thread workgroups, not three of 256).
+int row_threads(int64_t units_per_row)
+{
+    for (int t = 256; t >= 64; t /= 2)
+        if (units_per_row % t == 0) return t;
+    return 256;
+}
+
 // Grid of the row-walking kernels: x covers a row's units (at most 4096 workgroups,
 // the kernels stride beyond), y the rows (at most 65535, likewise).
-dim3 row_grid(int64_t M, int64_t units_per_row)
+dim3 row_grid(int64_t M, int64_t units_per_row, int threads)
 {
-    int64_t gx = (units_per_row + 255) / 256, gy = M;
+    int64_t gx = (units_per_row + threads - 1) / threads, gy = M;
     gx = gx < 1 ? 1 : (gx > 4096 ? 4096 : gx);
     gy = gy < 1 ? 1 : (gy > 65535 ? 65535 : gy);
     return dim3((unsigned)gx, (unsigned)gy);
@@ -223,11 +233,13 @@ int launch_noise(float* eta, int64_t ld_eta, int64_t M, int64_t K, int mech, dou
     const int64_t work = M * (K / 4);
     if (work == 0) return SPLITEE_OK;
     const bool pair = work < PAIR_BELOW;
-    const dim3 g = row_grid(M, K / (pair ? 2 : 4));
+    const int64_t upr = K / (pair ? 2 : 4);
+    const int nt = row_threads(upr);
+    const dim3 g = row_grid(M, upr, nt);
     if (pair)
-        hipLaunchKernelGGL(noise_kernel<true>, g, dim3(256), 0, s, eta, ld_eta, M, K, mech, scale, seed, sid, row0);
+        hipLaunchKernelGGL(noise_kernel<true>, g, dim3(nt), 0, s, eta, ld_eta, M, K, mech, scale, seed, sid, row0);
     else
-        hipLaunchKernelGGL(noise_kernel<false>, g, dim3(256), 0, s, eta, ld_eta, M, K, mech, scale, seed, sid, row0);
+        hipLaunchKernelGGL(noise_kernel<false>, g, dim3(nt), 0, s, eta, ld_eta, M, K, mech, scale, seed, sid, row0);
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
@@ -240,7 +252,9 @@ int launch_mask(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, i
     if (work == 0 && zero_count == 0) return SPLITEE_OK;
     const bool gen = eta == nullptr;
     const bool pair = gen && work < PAIR_BELOW;
-    const dim3 g = row_grid(M, K / (pair ? 2 : 4)), b(256);
+    const int64_t upr = K / (pair ? 2 : 4);
+    const int nt = row_threads(upr);
+    const dim3 g = row_grid(M, upr, nt), b(nt);
 #define SPLITEE_MASK_LAUNCH(P, G, PR)                                                                  \
     hipLaunchKernelGGL((mask_kernel<P, G, PR>), g, b, 0, s, X, ldx, eta, ld_eta, gen_mech, scale, seed, \
                        sid, row0, Xt, ldxt, plane_stride, M, K, zero_ptr, zero_count)

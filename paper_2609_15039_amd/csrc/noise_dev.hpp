@@ -27,9 +27,9 @@ __device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1
 {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-        uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-        c = u32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+        // the full 64-bit products: one v_mad_u64_u32 each instead of a mul_lo / mul_hi pair
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c.x, p1 = (uint64_t)0xCD9E8D57u * c.z;
+        c = u32x4{(uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0};
         k0 += 0x9E3779B9u;
         k1 += 0xBB67AE85u;
     }
@@ -205,23 +205,20 @@ __device__ __forceinline__ float round_dd_f32(dd v)
 
 // RN32(r) is the correctly rounded value of the real function whenever the true
 // value lies within |r| 2^-48 of r and no binary32 midpoint lies that close to r.
-// With f = RN32(r) and e = |r| - |f| (exact: the two are within one binary32 ulp),
-// the midpoints next to f lie h_up = ulp(f) / 2 above |f| and h_dn below it, h_dn =
-// ulp(f) / 4 when |f| is a power of two (the spacing halves below it), else ulp(f) / 2;
-// h_up - e and h_dn + e are the distances from |r| to them, exact (Sterbenz) since
-// each midpoint is within a factor 2 of |r|.  Zero, subnormal and non-finite f take
-// the slow path.
+// In the binade [2^E, 2^(E+1)) of r the binary32 midpoints are the odd multiples of
+// 2^(E-24), i.e. the binary64 values whose low 29 significand bits read 2^28, and
+// |r| 2^-48 < 2^(E-47) is 32 units of r's last place, 2^(E-52); the nearest midpoint
+// outside the binade is at least 2^(E-25) away.  So r is safe iff its low 29 bits
+// differ from 2^28 by more than 32 (an exact integer test), provided RN32(r) is a
+// normal binary32 number (else the slow path).
 __device__ __forceinline__ bool round_f32_safe(double r, float& out)
 {
-    const float f = (float)r;
-    out = f;
-    const uint32_t fb = __float_as_uint(f) & 0x7FFFFFFFu;
-    const double ar = fabs(r);
-    const double e = ar - (double)__uint_as_float(fb);
-    const double h_up = (double)__uint_as_float(fb & 0x7F800000u) * 0x1p-24;
-    const double h_dn = (fb & 0x007FFFFFu) ? h_up : 0.5 * h_up;
-    const double d = fmin(h_up - e, h_dn + e);
-    return fb >= 0x00800000u && fb < 0x7F800000u && d > ar * 0x1p-48;
+    out = (float)r;
+    const uint64_t b = (uint64_t)__double_as_longlong(r);
+    const uint32_t lo = (uint32_t)b & 0x1FFFFFFFu;
+    const uint32_t ex = (uint32_t)(b >> 52) & 0x7FFu;
+    const uint32_t d = lo > 0x10000000u ? lo - 0x10000000u : 0x10000000u - lo;
+    return d > 32u && ex >= 1023u - 126u && ex <= 1023u + 126u;
 }
 
 // -------------------------------------- binary64 log, sin(pi x), cos(pi x): fast path
