@@ -1420,11 +1420,49 @@ constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 //   M > 128:  128 x 256, 2 x 4 waves, 2 ahead (variants 22, 23); 64 x 256 when the 128-row
 //             tiles take more than one round of 256 workgroups and half-height tiles end
 //             in a fuller last round (Qwen3-4B gate/up at 1024 tokens: 608 tiles, 3
-//             rounds, against 1216 half tiles, 2.5 rounds' work: 361 -> 334 us)
+//             rounds, against 1216 half tiles, 2.5 rounds' work: 361 -> 334 us); else
+//             128 x 192 on 4 x 2 waves (variants 28, 29) where split_cost says it is
+//             cheaper than 128 x 256 (a sweep of 2 x 4 and 4 x 2 waves on 64 x 256,
+//             128 x 128 and 128 x 256 tiles found no other shape faster on these
+//             projections)
 // The K split fills about 256 CUs, keeps at least ST_MIN_KT K tiles per split and
 // at most ST_MAX_KS splits; below that cap it takes the split count with the fewest
 // rounds of 256 workgroups times K tiles per split rounded up to whole turns of the
 // ring (the rest of a turn runs on zero tiles), the fewer splits on a tie.
+
+// The K split of the streamed kernel for `tiles` output tiles of `ktiles` K tiles and
+// its cost: the split count (at most ST_MAX_KS, at least ST_MIN_KT K tiles per split,
+// at most 256 workgroups) with the fewest rounds of 256 workgroups times K tiles per
+// split rounded up to whole ring turns, the fewer splits on a tie.
+std::pair<int, int64_t> stream_split(int tiles, int ktiles, int ring)
+{
+    int ks = 1;
+    int64_t best = ((int64_t)tiles + 255) / 256 * ((ktiles + ring - 1) / ring * ring);
+    if (ktiles > 0) {
+        int ks_max = 256 / tiles;
+        if (ks_max > ktiles / ST_MIN_KT) ks_max = ktiles / ST_MIN_KT;
+        if (ks_max > ST_MAX_KS) ks_max = ST_MAX_KS;
+        for (int c = 2; c <= ks_max; ++c) {
+            const int64_t kps = (ktiles + c - 1) / c;
+            const int64_t cost = ((int64_t)tiles * c + 255) / 256 * ((kps + ring - 1) / ring * ring);
+            if (cost < best) { best = cost; ks = c; }
+        }
+    }
+    return {ks, best};
+}
+
+// Work of the busiest CU for bm x bn tiles split as stream_split chooses: rounds of
+// workgroups times tile area times K tiles per split; ties go to fewer splits by
+// comparing the split counts second.
+int64_t split_cost(int64_t M, int64_t N, int64_t K, int bm, int bn, int ring, bool allow_split)
+{
+    const int tiles = (int)(((M + bm - 1) / bm) * ((N + bn - 1) / bn));
+    const int ktiles = (int)((K + 63) / 64);
+    const std::pair<int, int64_t> sp = allow_split ? stream_split(tiles, ktiles, ring)
+                                                   : std::pair<int, int64_t>{1, ((int64_t)tiles + 255) / 256 *
+                                                                                    ((ktiles + ring - 1) / ring * ring)};
+    return (sp.second * bm * bn) * 16 + sp.first;
+}
 
 bool use_stream(int prec, int w_type)
 {
@@ -1446,6 +1484,13 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool all
             p.bm = 64; p.bn = 256; p.variant = x3 ? 24 : 25;
         } else {
             p.bm = 128; p.bn = 256; p.variant = x3 ? 22 : 23;
+            // 128 x 192 tiles on 4 x 2 waves when they cost less by split_cost (rounds of
+            // workgroups times tile area times K tiles per split): Qwen3-4B QKV at 1024
+            // tokens, 192 tiles of 128 x 256 on 256 CUs against exactly 256 of 128 x 192
+            // (116 -> 100 us); Llama-3.2-3B QKV, O and Down at 512 tokens by 1-6%
+            if (split_cost(M, N, K, 128, 192, 3, allow_split) < split_cost(M, N, K, 128, 256, 3, allow_split)) {
+                p.bn = 192; p.variant = x3 ? 28 : 29;
+            }
         }
     } else if (M <= 64) {
         p.bm = 64; p.bn = 256; p.variant = x3 ? 11 : 13;
@@ -1460,18 +1505,7 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool all
     const int tiles = p.mtiles * p.ntiles;
     // ring stages (K tiles in flight + 1) of the variant
     const int ring = (p.variant == 11 || p.variant == 13 || p.variant == 26 || p.variant == 27) ? 4 : 3;
-    int ks = 1;
-    if (allow_split && p.ktiles > 0) {
-        int ks_max = 256 / tiles;
-        if (ks_max > p.ktiles / ST_MIN_KT) ks_max = p.ktiles / ST_MIN_KT;
-        if (ks_max > ST_MAX_KS) ks_max = ST_MAX_KS;
-        int64_t best = -1;
-        for (int c = 1; c <= ks_max; ++c) {
-            const int64_t kps = (p.ktiles + c - 1) / c;
-            const int64_t cost = ((int64_t)tiles * c + 255) / 256 * ((kps + ring - 1) / ring * ring);
-            if (best < 0 || cost < best) { best = cost; ks = c; }
-        }
-    }
+    const int ks = allow_split ? stream_split(tiles, p.ktiles, ring).first : 1;
     p.kt_per_split = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
     p.ksplit = p.ktiles > 0 ? (p.ktiles + p.kt_per_split - 1) / p.kt_per_split : 1;
     p.counter_bytes = 0; // the partials are summed by a second kernel: no counters
@@ -1729,6 +1763,8 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         case 24: ST_LAUNCH(3, 64, 256, 1, 2, 8, true); break;
         case 25: ST_LAUNCH(1, 64, 256, 1, 2, 8, true); break;
         case 26: ST_LAUNCH(3, 64, 128, 2, 3, 8, true); break;
+        case 28: ST_LAUNCH(3, 128, 192, 4, 2, 8, true); break;
+        case 29: ST_LAUNCH(1, 128, 192, 4, 2, 8, true); break;
         default: ST_LAUNCH(1, 64, 128, 2, 3, 8, true); break;
         }
         if (p.ksplit > 1) {
@@ -1741,6 +1777,7 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
             case 14: case 15: ST_SUM(128, 128, 2, 2); break;
             case 22: case 23: ST_SUM(128, 256, 2, 4); break;
             case 24: case 25: ST_SUM(64, 256, 1, 8); break;
+            case 28: case 29: ST_SUM(128, 192, 4, 2); break;
             default: ST_SUM(64, 128, 2, 4); break;
             }
         }
