@@ -87,6 +87,26 @@ def test_tiled_fused_within_theorem4_gate(prec, M, N, K):
 
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
+def test_tiled_half_height_tiles_above_128_rows(prec):
+    # more than 256 tiles of 128 x 256 whose 64-row halves end in a fuller last round:
+    # 64 x 256 tiles on 4-wave workgroups, ragged in M (300 = 4 x 64 + 44), N (22052 =
+    # 86 x 256 + 36; row pitches are whole 16-byte units) and K (200 = 3 x 64 + 8)
+    err, b, cerr, cbound = _tiled_case(300, 22052, 200, prec, delta=825.27, eps=2.0, row0=7)
+    assert np.all(cerr <= cbound), "correction outside the dot-product bound"
+    assert np.all(err <= b["gate"]), "max err/gate %.3g" % np.max(err / b["gate"])
+    # the same plan on small integers: every element exact, so a misplaced tile shows
+    gp, _ = PREC[prec]
+    M, N, K = 300, 22052, 200
+    X = WL.gen_int((M, K), -8, 8, 40)
+    eta = WL.gen_int((M, K), -8, 8, 41)
+    W = WL.gen_int((N, K), -4, 4, 42)
+    T = sp.tile_weights(dev(W).to(torch.bfloat16))
+    Cd = dev(O.gemm64(eta, W).astype(np.float32))
+    Y = sp.masked_linear_fused(dev(X), T, Cd, sp.SPLITEE_MECH_NONE, 1.0, 1.0, 0, 0, 0, gp, eta_override=dev(eta))
+    assert np.array_equal(host(Y).astype(np.float64), O.gemm64(X, W))
+
+
+@pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
 @pytest.mark.parametrize("M,N,K", [(37, 100, 264), (130, 300, 1032), (1, 16, 8), (300, 520, 200)])
 def test_tiled_masked_linear_within_dot_bound(prec, M, N, K):
     gp, op = PREC[prec]
