@@ -72,6 +72,8 @@ def parse():
                          "vector-ALU GEMV reads whole rows), tiled otherwise (gate/up and the LM heads "
                          "at one or two tokens; 'mixed' when a workload has both)")
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of HIP graphs")
+    ap.add_argument("--step-masks-max-m", type=int, default=STEP_MASKS_MAX_M,
+                    help="up to this many tokens, draw the masks of a step in one launch")
     ap.add_argument("--no-modes", action="store_true", help="skip the other precision modes")
     ap.add_argument("--no-legs", action="store_true",
                     help="skip the other workloads measured beside the default one")
@@ -98,6 +100,7 @@ WORKLOADS = ["llama3b-layer-m128", "single-fp32-m32", "llama3b-28l-m512", "qwen3
              "qwen3-4b-decode-m1", "qwen3-4b-decode-m4", "qwen3-4b-decode-m16", "qwen3-4b-decode-m64",
              "llama3b-lmhead-m1", "llama3b-lmhead-m15", "llama3b-lmhead-m128",
              "qwen3-4b-lmhead-m1", "qwen3-4b-lmhead-m15"]
+STEP_MASKS_MAX_M = 16  # up to this many tokens the masks of a step are drawn in one launch
 DECODE_POS = 1024  # decode position t: rows [t, t+M) of the 2048-position correction bank
 
 
@@ -130,11 +133,14 @@ class Path:
     group, the weights, the precomputed correction rows and the outputs.
 
     Prefill-sized M: per projection, noise + mask in one kernel, then the GEMM with
-    the unmask epilogue.  Decode-sized M (the skinny kernel): per layer, one launch
-    draws the masks of all projection groups, then one launch per projection forms
-    fl32(X + eta), multiplies and unmasks."""
+    the unmask epilogue.  Up to `step_masks_max_m` tokens the noise does not fill the
+    chip one projection at a time, so one launch per step draws the masks of every
+    layer and projection group (the noise does not depend on the input), and the
+    fused call of each projection forms fl32(X + eta) from the drawn mask: inside the
+    skinny GEMM at M <= 16, by the mask kernel ahead of the streamed GEMM above."""
 
-    def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets, layout="auto"):
+    def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets, layout="auto",
+                 step_masks_max_m=STEP_MASKS_MAX_M):
         self.torch, self.sp = torch, sp
         self.prec, self.mech, self.delta, self.eps = prec, mech, delta, eps
         (self.projs, self.M, self.layers_per_step, nsets, self.w_dtype, bank_rows,
@@ -159,12 +165,12 @@ class Path:
             dt = torch.float32 if prec == sp.SPLITEE_PREC_F32 else torch.int16
             self.Xt.append(torch.empty((planes, M, p.K), dtype=dt, device=dev))
             self.Y.append(torch.empty((M, p.N), dtype=torch.float32, device=dev))
-        self.decode = M <= 16 and prec != sp.SPLITEE_PREC_F32
+        self.step_masks = M <= step_masks_max_m and prec != sp.SPLITEE_PREC_F32
         for p in self.projs:
-            self.ws.append(sp.workspace(M, p.N, p.K, prec, dev, gemm_only=not self.decode))
-        # decode: the masks of every layer of a step, [layer][token][k] per projection group
+            self.ws.append(sp.workspace(M, p.N, p.K, prec, dev, gemm_only=not self.step_masks))
+        # drawn per step: the masks of every layer of a step, [layer][token][k] per projection group
         self.eta = [torch.empty((self.layers_per_step, M, p.K), dtype=torch.float32, device=dev)
-                    for p in self.projs] if self.decode else None
+                    for p in self.projs] if self.step_masks else None
         self.sid_step = WL.stream_id(1, 0) - WL.stream_id(0, 0)
         self.W, self.C, self.sid = [], [], []
         for l in range(nlayers):
@@ -199,10 +205,10 @@ class Path:
 
     def gemm(self, l, i):
         """The GEMM + unmask launch of projection group i of layer (or weight set) l
-        (decode: mask + GEMM + unmask, on the mask drawn for the layer)."""
+        (masks drawn per step: mask + GEMM + unmask, on the mask drawn for the layer)."""
         p, M = self.projs[i], self.M
         W, C = self.W[l][i], self.C[l][i]
-        if self.decode:
+        if self.step_masks:
             self.sp.splitee_masked_linear_fused(
                 self.X[i], p.K, W, self.wt[i], p.K, C, C.stride(0), self.Y[i], p.N, M, p.N, p.K, self.mech,
                 self.delta, self.eps, 0, self.sid[l][i], self.row0, self.eta[i][l % self.layers_per_step], self.prec,
@@ -213,7 +219,7 @@ class Path:
                                                  self.ws[i][0], self.ws[i][1])
 
     def draw_masks(self, base):
-        """Decode: one launch draws the masks of all layers and projection groups of a step."""
+        """Masks drawn per step: one launch draws the masks of all layers and projection groups of a step."""
         Ks = [p.K for p in self.projs]
         self.sp.splitee_noise_gen_multi(self.eta, Ks, Ks, self.sid[base], self.M, self.mech, self.delta,
                                         self.eps, 0, self.row0, reps=self.layers_per_step,
@@ -228,11 +234,11 @@ class Path:
     def launches(self, s):
         """All kernels of step s: noise, mask, GEMM and unmask of every projection."""
         base = (s % self.nsets) * self.layers_per_step
-        if self.decode:
+        if self.step_masks:
             self.draw_masks(base)
         for l in range(base, base + self.layers_per_step):
             for i in range(len(self.projs)):
-                if not self.decode:
+                if not self.step_masks:
                     self.mask(l, i)
                 self.gemm(l, i)
 
@@ -241,15 +247,15 @@ class Path:
 
     def gemm_bytes(self):
         """Algorithmic bytes of each GEMM + unmask launch: W, float32 X (and, in the
-        decode launch that forms the masked input, float32 eta), C and Y."""
+        fused call that forms the masked input from a drawn mask, float32 eta), C and Y."""
         wb = 4.0 if self.w_dtype == "f32" else 2.0
-        xb = 8.0 if self.decode else 4.0
+        xb = 8.0 if self.step_masks else 4.0
         return [wb * p.N * p.K + xb * self.M * p.K + 8.0 * self.M * p.N for p in self.projs]
 
 
 def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
     path = Path(torch, sp, WL, name, prec, sp.MECHS[args.mech], args.delta, args.eps,
-                args.weight_sets, args.layout)
+                args.weight_sets, args.layout, args.step_masks_max_m)
     nsets = path.nsets
     graphs = None
     if not args.no_graph:
@@ -295,8 +301,8 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
         del timed
 
     # per-launch duration of the GEMM + unmask kernel of each projection group, and of the
-    # noise + mask launch (prefill: per projection group; decode: the one launch per step
-    # that draws every layer's masks): the launches for every layer / weight set of the run,
+    # noise + mask launch (per projection group, or the one launch per step that draws
+    # every layer's masks): the launches for every layer / weight set of the run,
     # back to back in one HIP graph (eager launches when --no-graph), bracketed by HIP
     # events recorded on the stream the kernels run on; averaged over launches and repeats
     nproj = len(path.projs)
@@ -330,7 +336,7 @@ def run_mode(torch, sp, WL, name, prec, args, steps, warmup):
             f(l, i)
 
     per_proj_us = [time_launches(lambda i=i: each_layer(path.gemm, i), n_layers) for i in range(nproj)]
-    if path.decode:
+    if path.step_masks:
         # one launch per step: 16 of them per graph, so that the graph launch itself is amortised
         mask_us = [time_launches(lambda: [path.draw_masks((s % path.nsets) * path.layers_per_step)
                                           for s in range(16)], 16)]
@@ -508,8 +514,9 @@ def counter_launches(torch, sp, WL, args, prec):
     """The GEMM launches alone, for counter collection: after set-up, `n` rounds of
     one launch per projection group (layer 0), in projection order, each followed by
     a device synchronization; these are the run's last dispatches."""
-    path = Path(torch, sp, WL, args.workload, prec, sp.MECHS[args.mech], args.delta, args.eps, 1, args.layout)
-    if path.decode:
+    path = Path(torch, sp, WL, args.workload, prec, sp.MECHS[args.mech], args.delta, args.eps, 1, args.layout,
+                args.step_masks_max_m)
+    if path.step_masks:
         path.draw_masks(0)
     else:
         for i, p in enumerate(path.projs):
@@ -719,19 +726,19 @@ def leg_summary(sp, path, ms, per_proj_us, mask_us, prec, workload):
     pname = {v: k for k, v in sp.PRECS.items()}[prec]
     traffic = measured_traffic(workload, pname, path.layout, [p.name for p in projs])
     roof.update({"kernel": ("%s projection: mask + GEMM + unmask in one launch (masks drawn per step)"
-                            if path.decode else "%s projection: GEMM + unmask launch") % projs[d].name,
+                            if path.step_masks else "%s projection: GEMM + unmask launch") % projs[d].name,
                  "launch_us": round(per_proj_us[d], 2), "algorithmic_bytes": int(gb[d]),
                  "algorithmic_flops": int(flops[d]), "algorithmic_ai": round(flops[d] / gb[d], 1),
                  "traffic": None if traffic is None else int(traffic[projs[d].name]),
                  "traffic_per_launch": traffic and {k: int(v) for k, v in traffic.items()}})
-    if not f32 and not path.decode:
+    if not f32 and M > 16:
         issued = planes * flops[d] / (per_proj_us[d] * 1e-6) / 1e12
         roof.update({"mfma_issued_tflops": round(issued, 1), "mfma_issued_frac": round(issued / BF16_PEAK_TFS, 4),
                      "mfma_passes": planes})
     step_flops = L * sum(flops)
     step_bytes = L * sum(gb)
     step = frac_of(step_flops, step_bytes, ms * 1e3)
-    mask_total_us = (mask_us[0] if path.decode else L * sum(mask_us))
+    mask_total_us = (mask_us[0] if path.step_masks else L * sum(mask_us))
     step.update({"what": "whole step: noise, mask, GEMM and unmask of every projection group of %d layer(s); "
                          "algorithmic flops and fused-minimum bytes over ms per step" % L,
                  "ms": round(ms, 4), "algorithmic_flops": int(step_flops), "algorithmic_bytes": int(step_bytes),
@@ -740,7 +747,7 @@ def leg_summary(sp, path, ms, per_proj_us, mask_us, prec, workload):
     roof["step"] = step
     roof["launches"] = {p.name: dict(frac_of(flops[i], gb[i], per_proj_us[i]), launch_us=round(per_proj_us[i], 2))
                         for i, p in enumerate(projs)}
-    roof["noise_mask_launch_us"] = ({"all layers": round(mask_us[0], 2)} if path.decode else
+    roof["noise_mask_launch_us"] = ({"all layers": round(mask_us[0], 2)} if path.step_masks else
                                     {p.name: round(u, 2) for p, u in zip(projs, mask_us)})
     value = step_flops / (ms * 1e-3) / 1e12
     return {"value": round(value, 3), "ms_per_step": round(ms, 4), "tokens": M, "layers_per_step": L,

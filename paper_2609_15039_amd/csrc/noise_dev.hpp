@@ -13,6 +13,7 @@
 // generates its masked-input slice itself.
 #pragma once
 #include "common.hpp"
+#include "noise_tables.hpp"
 #include <math.h>
 
 #pragma clang fp contract(off)
@@ -227,49 +228,46 @@ __device__ __forceinline__ bool round_f32_safe(double r, float& out)
 // x = (2w + 1) 2^-32.
 // Each stays within a few binary64 ulps (relative error about 2^-51), inside the
 // 2^-48 budget of round_f32_safe; the fast and slow paths of every transform are
-// compared on all 2^32 words.
+// compared on all 2^32 words.  Both reductions read a small table written by
+// gen_noise_tables.py (noise_tables.hpp).
 
 // ln 2 = LN2_HI + LN2_LO to about 2^-98; LN2_HI has 44 significant bits, so e LN2_HI
 // is exact for every binary64 exponent e.
 constexpr double LN2_HI = 0x1.62e42fefa38p-1;
 constexpr double LN2_LO = 0x1.ef35793c7673p-45;
-// pi = PI_HI + PI_LO to about 2^-74; PI_HI has 22 significant bits, so PI_HI r is exact
-// for r = k 2^-32, |k| <= 2^30.
+// pi = PI_HI + PI_LO to about 2^-74; PI_HI has 22 significant bits, so PI_HI d is exact
+// for d = k 2^-32, |k| <= 2^30.
 constexpr double PI_HI = 0x1.921fbp+1;
 constexpr double PI_LO = 0x1.5110b4611a626p-21;
 
-// log x = e ln 2 + log m for x = 2^e m, m in [sqrt(1/2), sqrt(2)); log m = 2 atanh(s),
-// s = (m - 1) / (m + 1), |s| < 0.1716, by the atanh series to s^21 (the first term
-// left out is below 2^-56 of the sum).  m - 1 is exact; s comes from a reciprocal
-// refined by two Newton steps and one correction of the quotient.
+// log x = e ln 2 - log rc + log1p(r) for x = 2^e m', with m' in [0.70703125, 1.4140625)
+// (the binary64 significand, halved when its top 7 fraction bits i are 53 or more),
+// rc the table's reciprocal of the centre of entry i (20 significant bits, or 1 next
+// to m' = 1) and r = m' rc - 1, exact because m' has at most 33 significant bits;
+// |r| <= 2^-7, so log1p(r) to r^8 leaves out less than 2^-59 of its value, and -log rc
+// comes from the table as hi + lo.  Near x = 1 (rc = 1) nothing cancels.
 __device__ __forceinline__ double log_fast(double x)
 {
     const uint64_t b = (uint64_t)__double_as_longlong(x);
     int e = (int)(b >> 52) - 1023;
+    const int i = (int)((b >> 45) & 127u);
     uint64_t mb = (b & 0x000FFFFFFFFFFFFFull) | 0x3FF0000000000000ull; // m in [1, 2)
-    if (mb >= 0x3FF6A09E667F3BCDull) { mb -= 0x0010000000000000ull; ++e; } // m > sqrt(2): halve
+    if (i >= 53) { mb -= 0x0010000000000000ull; ++e; }                 // m' = m / 2
     const double m = __longlong_as_double((long long)mb);
-    const double f = m - 1.0;
-    const double d = m + 1.0;
-    double y = __builtin_amdgcn_rcp(d);
-    y = fma(fma(-d, y, 1.0), y, y);
-    y = fma(fma(-d, y, 1.0), y, y);
-    double s = f * y;
-    s = fma(fma(-d, s, f), y, s);
-    const double z = s * s;
-    double p = 1.0 / 21.0;
-    p = fma(p, z, 1.0 / 19.0);
-    p = fma(p, z, 1.0 / 17.0);
-    p = fma(p, z, 1.0 / 15.0);
-    p = fma(p, z, 1.0 / 13.0);
-    p = fma(p, z, 1.0 / 11.0);
-    p = fma(p, z, 1.0 / 9.0);
-    p = fma(p, z, 1.0 / 7.0);
-    p = fma(p, z, 1.0 / 5.0);
-    p = fma(p, z, 1.0 / 3.0);
-    const double logm = 2.0 * fma(s * z, p, s); // 2 (s + s^3/3 + ... + s^21/21)
+    const double2 t0 = *reinterpret_cast<const double2*>(&NOISE_LOG_TABLE[i][0]); // rc, -log rc (hi)
+    const double t1 = NOISE_LOG_TABLE[i][2];                                       // -log rc (lo)
+    const double r = fma(m, t0.x, -1.0);
+    const double z = r * r;
+    double p = -1.0 / 8.0;
+    p = fma(p, r, 1.0 / 7.0);
+    p = fma(p, r, -1.0 / 6.0);
+    p = fma(p, r, 1.0 / 5.0);
+    p = fma(p, r, -0.25);
+    p = fma(p, r, 1.0 / 3.0);
+    p = fma(p, r, -0.5);
+    const double l1p = fma(z, p, r); // r - r^2/2 + r^3/3 - ... - r^8/8
     const double de = (double)e;
-    return fma(de, LN2_HI, fma(de, LN2_LO, logm));
+    return fma(de, LN2_HI, t0.y) + fma(de, LN2_LO, t1 + l1p);
 }
 
 // sqrt v for positive normal v, within about one binary64 ulp: the hardware
@@ -288,41 +286,42 @@ __device__ __forceinline__ double sqrt_fast(double v)
     return fma(fma(-g, g, v), h, g);
 }
 
-// sin(pi x) and cos(pi x) for x = (2w + 1) 2^-32 in (0, 2): x = q/2 + r with q the
-// nearest integer to 2x and |r| <= 1/4, both exact in integer arithmetic; then the
-// Taylor polynomials of sin and cos at pi r (|pi r| <= pi/4, the first terms left out
-// below 2^-54 of the value) and the quadrant's swap and signs.
+// sin(pi x) and cos(pi x) for x = (2w + 1) 2^-32 in (0, 2): x = q/2 + j/64 + d with q
+// the nearest integer to 2x, j the nearest integer to 64 (x - q/2) (|j| <= 16) and
+// |d| <= 2^-7, all three exact in integer arithmetic; sin and cos of pi d by Taylor
+// polynomials to degree 7 and 8 (|pi d| <= pi/128: the first terms left out are below
+// 2^-61 of the value), combined with the table's sin and cos of pi |j| / 64 by the
+// angle-sum formulas, then the quadrant's swap and signs.  For j = 0 the sine is
+// sin(pi d) itself; otherwise no more than one bit cancels.
 __device__ __forceinline__ void sincospi_fast(uint32_t w, double& sn, double& cs)
 {
-    const int64_t n = 2 * (int64_t)w + 1;          // x = n 2^-32
-    const int64_t q = (n + (1ll << 30)) >> 31;     // nearest integer to 2x (0..4)
-    const double r = (double)(n - (q << 31)) * 0x1p-32;
-    const double t = fma(PI_LO, r, PI_HI * r);     // pi r
+    // in 32-bit integers: 2x = (w + 1/2) 2^-30, so q = round(w 2^-30) = (w >> 30) + bit 29
+    // of w, and x - q/2 = rn 2^-32 with rn = 2 (w - q 2^30) + 1, |rn| <= 2^30 + 1
+    const uint32_t q = (w >> 30) + ((w >> 29) & 1u); // nearest integer to 2x (0..4)
+    const int32_t rn = 2 * (int32_t)(w - (q << 30)) + 1;
+    const int32_t j = (rn + (1 << 25)) >> 26;        // nearest integer to 64 rn 2^-32
+    const double d = (double)(rn - j * (1 << 26)) * 0x1p-32;
+    const double t = fma(PI_LO, d, PI_HI * d);     // pi d
     const double z = t * t;
-    double ps = 1.0 / 355687428096000.0;           // 1/17!
-    ps = fma(ps, z, -1.0 / 1307674368000.0);       // 1/15!
-    ps = fma(ps, z, 1.0 / 6227020800.0);           // 1/13!
-    ps = fma(ps, z, -1.0 / 39916800.0);            // 1/11!
-    ps = fma(ps, z, 1.0 / 362880.0);               // 1/9!
-    ps = fma(ps, z, -1.0 / 5040.0);                // 1/7!
+    double ps = -1.0 / 5040.0;                     // 1/7!
     ps = fma(ps, z, 1.0 / 120.0);                  // 1/5!
     ps = fma(ps, z, -1.0 / 6.0);                   // 1/3!
-    const double sr = fma(t * z, ps, t);           // sin(pi r)
-    double pc = -1.0 / 6402373705728000.0;         // 1/18!
-    pc = fma(pc, z, 1.0 / 20922789888000.0);       // 1/16!
-    pc = fma(pc, z, -1.0 / 87178291200.0);         // 1/14!
-    pc = fma(pc, z, 1.0 / 479001600.0);            // 1/12!
-    pc = fma(pc, z, -1.0 / 3628800.0);             // 1/10!
-    pc = fma(pc, z, 1.0 / 40320.0);                // 1/8!
+    const double st = fma(t * z, ps, t);           // sin(pi d)
+    double pc = 1.0 / 40320.0;                     // 1/8!
     pc = fma(pc, z, -1.0 / 720.0);                 // 1/6!
     pc = fma(pc, z, 1.0 / 24.0);                   // 1/4!
     pc = fma(pc, z, -0.5);                         // 1/2!
-    const double cr = fma(z, pc, 1.0);             // cos(pi r)
+    const double ct = fma(z, pc, 1.0);             // cos(pi d)
+    const int a = (int)(j < 0 ? -j : j);
+    const double2 tab = *reinterpret_cast<const double2*>(&NOISE_SINCOS_TABLE[a][0]);
+    const double S = j < 0 ? -tab.x : tab.x, C = tab.y;
+    const double sr = fma(S, ct, C * st);          // sin(pi (j/64 + d))
+    const double cr = fma(C, ct, -(S * st));       // cos(pi (j/64 + d))
     // sin(pi (q/2 + r)), cos(pi (q/2 + r)) by q mod 4
     const int qq = (int)(q & 3);
-    const double a = (qq & 1) ? cr : sr, c = (qq & 1) ? sr : cr;
-    sn = (qq & 2) ? -a : a;
-    cs = (qq == 1 || qq == 2) ? -c : c;
+    const double sa = (qq & 1) ? cr : sr, ca = (qq & 1) ? sr : cr;
+    sn = (qq & 2) ? -sa : sa;
+    cs = (qq == 1 || qq == 2) ? -ca : ca;
 }
 
 // ---------------------------------------------------- the four transforms

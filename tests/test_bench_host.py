@@ -55,12 +55,12 @@ class _FakeSp:
 
 
 class _FakePath:
-    def __init__(self, M, decode, projs, layers):
-        self.projs, self.M, self.decode, self.layers_per_step = projs, M, decode, layers
+    def __init__(self, M, step_masks, projs, layers):
+        self.projs, self.M, self.step_masks, self.layers_per_step = projs, M, step_masks, layers
         self.w_dtype, self.layout, self.tiled, self.nsets, self.row0 = "bf16", "tiled", [True] * len(projs), 1, 0
 
     def gemm_bytes(self):
-        return [2.0 * p.N * p.K + (8.0 if self.decode else 4.0) * self.M * p.K + 8.0 * self.M * p.N
+        return [2.0 * p.N * p.K + (8.0 if self.step_masks else 4.0) * self.M * p.K + 8.0 * self.M * p.N
                 for p in self.projs]
 
 
