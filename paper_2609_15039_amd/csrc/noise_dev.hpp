@@ -150,8 +150,10 @@ __device__ void dd_sincos_2pi_small(double f, dd& sn, dd& cs)
 }
 
 // sin and cos of 2 pi u(w) in double-double: octant reduction of the exact
-// u = j / 2^33 (j = 2w + 1), then the series on an argument in [0, pi/4].
-__device__ __attribute__((noinline)) void dd_sincos_2pi(uint32_t w, dd& sn, dd& cs)
+// u = j / 2^33 (j = 2w + 1), then the series on an argument in [0, pi/4].  Returned
+// by value (in registers), so that the kernels that call it need no scratch memory.
+struct dd_pair { dd s, c; };
+__device__ __attribute__((noinline)) dd_pair dd_sincos_2pi(uint32_t w)
 {
     uint64_t j = 2ull * (uint64_t)w + 1ull;
     int oct = (int)(j >> 30);
@@ -173,8 +175,7 @@ __device__ __attribute__((noinline)) void dd_sincos_2pi(uint32_t w, dd& sn, dd& 
     case 6: s = dd_neg(c1); c = s1;         break;
     default: s = dd_neg(s1); c = c1;        break;
     }
-    sn = s;
-    cs = c;
+    return dd_pair{s, c};
 }
 
 // --------------------------------------------------- rounding to binary32
@@ -353,10 +354,9 @@ __device__ __forceinline__ void cr_sincos_2pi(uint32_t w, bool force_slow, float
     bool ok_s = !force_slow && round_f32_safe(s64, sn);
     bool ok_c = !force_slow && round_f32_safe(c64, cs);
     if (!(ok_s && ok_c)) {
-        dd s, c;
-        dd_sincos_2pi(w, s, c);
-        if (!ok_s) sn = round_dd_f32(s);
-        if (!ok_c) cs = round_dd_f32(c);
+        const dd_pair p = dd_sincos_2pi(w);
+        if (!ok_s) sn = round_dd_f32(p.s);
+        if (!ok_c) cs = round_dd_f32(p.c);
     }
 }
 
