@@ -1420,9 +1420,9 @@ constexpr int TARGET_WGS = 512; // two workgroups per CU on 256 CUs
 //   M > 128:  128 x 256, 2 x 4 waves, 2 ahead (variants 22, 23); 64 x 256 when the 128-row
 //             tiles take more than one round of 256 workgroups and half-height tiles end
 //             in a fuller last round (Qwen3-4B gate/up at 1024 tokens: 608 tiles, 3
-//             rounds, against 1216 half tiles, 2.5 rounds' work: 361 -> 334 us), on 4
-//             waves of 64 x 64 in workgroups of their own, two per CU (variants 30, 31:
-//             each workgroup waits at its own barrier, so one's loads run under the
+//             rounds, against 1216 half tiles, 2.5 rounds' work: 361 -> 334 us), for three
+//             planes on 4 waves of 64 x 64 in workgroups of their own, two per CU (variant
+//             30: each workgroup waits at its own barrier, so one's loads run under the
 //             other's MFMAs, and a masked-input fragment feeds two MFMAs instead of one;
 //             the same gate/up 332 -> 287 us against 8 waves side by side); else
 //             128 x 192 on 4 x 2 waves (variants 28, 29) where split_cost says it is
@@ -1485,8 +1485,9 @@ Plan plan_stream(int64_t M, int64_t N, int64_t K, int prec, int w_type, bool all
             p.bm = 64; p.bn = 256; p.variant = x3 ? 24 : 25;
         } else if (const int64_t t128 = (M + 127) / 128 * ((N + 255) / 256), t64 = (M + 63) / 64 * ((N + 255) / 256);
                    t128 > 256 && (t64 + 255) / 256 < 2 * ((t128 + 255) / 256)) {
-            // half-height tiles on 4 waves, two workgroups per CU (72 KB of LDS each)
-            p.bm = 64; p.bn = 256; p.variant = x3 ? 30 : 31;
+            // three planes: half-height tiles on 4 waves, two workgroups per CU (72 KB of LDS
+            // each); one plane keeps 8 waves (its gate/up at 1024 tokens: 170 us against 212)
+            p.bm = 64; p.bn = 256; p.variant = x3 ? 30 : 25;
         } else {
             p.bm = 128; p.bn = 256; p.variant = x3 ? 22 : 23;
             // 128 x 192 tiles on 4 x 2 waves when they cost less by split_cost (rounds of
@@ -1771,7 +1772,6 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         case 28: ST_LAUNCH(3, 128, 192, 4, 2, 8, true); break;
         case 29: ST_LAUNCH(1, 128, 192, 4, 2, 8, true); break;
         case 30: ST_LAUNCH(3, 64, 256, 1, 2, 4, true); break;
-        case 31: ST_LAUNCH(1, 64, 256, 1, 2, 4, true); break;
         default: ST_LAUNCH(1, 64, 128, 2, 3, 8, true); break;
         }
         if (p.ksplit > 1) {
@@ -1785,7 +1785,7 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
             case 22: case 23: ST_SUM(128, 256, 2, 4); break;
             case 24: case 25: ST_SUM(64, 256, 1, 8); break;
             case 28: case 29: ST_SUM(128, 192, 4, 2); break;
-            case 30: case 31: ST_SUM(64, 256, 1, 4); break;
+            case 30: ST_SUM(64, 256, 1, 4); break;
             default: ST_SUM(64, 128, 2, 4); break;
             }
         }
