@@ -155,7 +155,7 @@ class Path:
         g.manual_seed(1)
         wt = sp.SPLITEE_F32 if self.w_dtype == "f32" else sp.SPLITEE_BF16
         can_tile = wt == sp.SPLITEE_BF16 and prec != sp.SPLITEE_PREC_F32
-        self.tiled = [can_tile and weight_tiled(layout, M, p.N) for p in self.projs]
+        self.tiled = [can_tile and weight_tiled(layout, M, p.N, p.K) for p in self.projs]
         self.wt = [sp.SPLITEE_BF16_TILED if t else wt for t in self.tiled]
         self.layout = "tiled" if all(self.tiled) else ("row-major" if not any(self.tiled) else "mixed")
         self.X, self.Xt, self.Y, self.ws = [], [], [], []
@@ -477,13 +477,21 @@ def gemm_source_sha():
     return h.hexdigest()
 
 
-def weight_tiled(layout, M, N):
-    """Whether a bfloat16 projection of N output rows at M tokens stores W tiled.  auto:
-    one or two tokens run the vector-ALU GEMV, which reads whole rows of row-major W faster
-    for the narrower projections and 32-row blocks of tiled W faster from 16384 rows up
-    (gate/up, the LM heads); every other M runs the MFMA kernels on tiled W."""
+def weight_tiled(layout, M, N, K):
+    """Whether a bfloat16 projection of N output rows and K columns at M tokens stores W
+    tiled.  auto: one or two tokens run a vector-ALU GEMV, on row-major W (whole rows per
+    wave) or on tiled W (32-row blocks); measured on the Llama-3.2-3B and Qwen3-4B
+    projections and on 2560-24576 x 2560-4096 matrices, the tiled one is faster from 8192
+    rows up at one token (8192 x 3072: 12.9 -> 12.1 us, Llama-3.2-3B gate/up 21.9 -> 19.4 us;
+    at 6144 rows a tie) and from about 12 M elements up at two (Qwen3-4B Down 20.2 -> 15.3 us),
+    the row-major one below (Qwen3-4B O at one token 7.1 us against 9.0); every other M runs
+    the MFMA kernels on tiled W."""
     if layout == "auto":
-        return not (M <= 2 and N < 16384)
+        if M == 1:
+            return N >= 8192
+        if M == 2:
+            return N * K >= 12 * 2**20
+        return True
     return layout == "tiled"
 
 

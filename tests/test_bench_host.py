@@ -18,13 +18,18 @@ def test_more_than_one_gpu_is_refused():
 
 def test_weight_layout_rule():
     # auto: row-major only for one or two tokens of matrices under 16384 rows
-    assert not bench.weight_tiled("auto", 1, 6144)
-    assert not bench.weight_tiled("auto", 2, 16383)
-    assert bench.weight_tiled("auto", 1, 19456)      # Qwen3-4B gate/up
-    assert bench.weight_tiled("auto", 1, 128256)     # Llama-3.2-3B LM head
-    assert bench.weight_tiled("auto", 3, 2560)
-    assert bench.weight_tiled("tiled", 1, 8)
-    assert not bench.weight_tiled("row-major", 512, 5120)
+    assert not bench.weight_tiled("auto", 1, 5120, 3072)   # Llama-3.2-3B QKV
+    assert not bench.weight_tiled("auto", 1, 2560, 9728)   # Qwen3-4B Down: wide K, few rows
+    assert not bench.weight_tiled("auto", 1, 6144, 2560)   # Qwen3-4B QKV: a tie, row-major kept
+    assert bench.weight_tiled("auto", 1, 8192, 3072)
+    assert bench.weight_tiled("auto", 1, 19456, 2560)      # Qwen3-4B gate/up
+    assert bench.weight_tiled("auto", 1, 128256, 3072)     # Llama-3.2-3B LM head
+    assert not bench.weight_tiled("auto", 2, 2560, 4096)   # Qwen3-4B O: 10.5 M elements
+    assert bench.weight_tiled("auto", 2, 5120, 2560)       # 13.1 M elements
+    assert bench.weight_tiled("auto", 2, 2560, 9728)       # Qwen3-4B Down at two tokens
+    assert bench.weight_tiled("auto", 3, 2560, 2560)
+    assert bench.weight_tiled("tiled", 1, 8, 8)
+    assert not bench.weight_tiled("row-major", 512, 5120, 3072)
 
 
 def _summary(tmp_path, sha, rows):
