@@ -287,21 +287,20 @@ __device__ __forceinline__ double sqrt_fast(double v)
     return fma(fma(-g, g, v), h, g);
 }
 
-// sin(pi x) and cos(pi x) for x = (2w + 1) 2^-32 in (0, 2): x = q/2 + j/64 + d with q
-// the nearest integer to 2x, j the nearest integer to 64 (x - q/2) (|j| <= 16) and
-// |d| <= 2^-7, all three exact in integer arithmetic; sin and cos of pi d by Taylor
-// polynomials to degree 7 and 8 (|pi d| <= pi/128: the first terms left out are below
-// 2^-61 of the value), combined with the table's sin and cos of pi |j| / 64 by the
-// angle-sum formulas, then the quadrant's swap and signs.  For j = 0 the sine is
-// sin(pi d) itself; otherwise no more than one bit cancels.
+// sin(pi x) and cos(pi x) for x = (2w + 1) 2^-32 in (0, 2): x = j/64 + d with j the nearest
+// integer to 64x (0..128) and |d| <= 2^-7 + 2^-32, both exact in 32-bit integer arithmetic;
+// sin and cos of pi d by Taylor polynomials to degree 7 and 8 (|pi d| <= pi/128: the first
+// terms left out are below 2^-61 of the value), combined with the table's sin and cos of
+// pi j / 64 (the whole circle, exact zeros) by the angle-sum formulas.  Next to a zero of sin
+// or cos the table's entry there is 0 and the result is +-sin(pi d) itself; elsewhere no more
+// than one bit cancels.
 __device__ __forceinline__ void sincospi_fast(uint32_t w, double& sn, double& cs)
 {
-    // in 32-bit integers: 2x = (w + 1/2) 2^-30, so q = round(w 2^-30) = (w >> 30) + bit 29
-    // of w, and x - q/2 = rn 2^-32 with rn = 2 (w - q 2^30) + 1, |rn| <= 2^30 + 1
-    const uint32_t q = (w >> 30) + ((w >> 29) & 1u); // nearest integer to 2x (0..4)
-    const int32_t rn = 2 * (int32_t)(w - (q << 30)) + 1;
-    const int32_t j = (rn + (1 << 25)) >> 26;        // nearest integer to 64 rn 2^-32
-    const double d = (double)(rn - j * (1 << 26)) * 0x1p-32;
+    // 64x = (w + 1/2) 2^-25, so j = (w >> 25) + bit 24 of w, and x - j/64 = dn 2^-32 with
+    // dn = 2 (w - j 2^25) + 1 (j 2^25 taken modulo 2^32: j = 128 only for w near 2^32)
+    const uint32_t j = (w >> 25) + ((w >> 24) & 1u);
+    const int32_t dn = 2 * (int32_t)(w - (j << 25)) + 1;
+    const double d = (double)dn * 0x1p-32;
     const double t = fma(PI_LO, d, PI_HI * d);     // pi d
     const double z = t * t;
     double ps = -1.0 / 5040.0;                     // 1/7!
@@ -313,16 +312,9 @@ __device__ __forceinline__ void sincospi_fast(uint32_t w, double& sn, double& cs
     pc = fma(pc, z, 1.0 / 24.0);                   // 1/4!
     pc = fma(pc, z, -0.5);                         // 1/2!
     const double ct = fma(z, pc, 1.0);             // cos(pi d)
-    const int a = (int)(j < 0 ? -j : j);
-    const double2 tab = *reinterpret_cast<const double2*>(&NOISE_SINCOS_TABLE[a][0]);
-    const double S = j < 0 ? -tab.x : tab.x, C = tab.y;
-    const double sr = fma(S, ct, C * st);          // sin(pi (j/64 + d))
-    const double cr = fma(C, ct, -(S * st));       // cos(pi (j/64 + d))
-    // sin(pi (q/2 + r)), cos(pi (q/2 + r)) by q mod 4
-    const int qq = (int)(q & 3);
-    const double sa = (qq & 1) ? cr : sr, ca = (qq & 1) ? sr : cr;
-    sn = (qq & 2) ? -sa : sa;
-    cs = (qq == 1 || qq == 2) ? -ca : ca;
+    const double2 tab = *reinterpret_cast<const double2*>(&NOISE_SINCOS_TABLE[j][0]);
+    sn = fma(tab.x, ct, tab.y * st);               // sin(pi (j/64 + d))
+    cs = fma(tab.y, ct, -(tab.x * st));            // cos(pi (j/64 + d))
 }
 
 // ---------------------------------------------------- the four transforms

@@ -64,13 +64,20 @@ def test_log_reduction_entries():
 
 def test_sincos_entries():
     _, _, sc = _tables()
-    assert len(sc) == 17
-    assert sc[0] == (0.0, 1.0) and sc[16][0] == sc[16][1]
+    assert len(sc) == 129
+    # the zeros and units of the whole circle exactly
+    for j, v in ((0, (0.0, 1.0)), (32, (1.0, 0.0)), (64, (0.0, -1.0)), (96, (-1.0, 0.0)), (128, (0.0, 1.0))):
+        assert sc[j] == v, j
+    assert sc[16][0] == sc[16][1]
     for j, (s, c) in enumerate(sc):
-        assert abs(s - math.sin(math.pi * j / 64)) <= math.ulp(max(s, 1e-300))
-        assert abs(c - math.cos(math.pi * j / 64)) <= math.ulp(c)
+        # math.sin / math.cos of the binary64 angle: within a few units of 2^-53 of the entry
+        assert abs(s - math.sin(math.pi * j / 64)) <= 2.0 ** -50
+        assert abs(c - math.cos(math.pi * j / 64)) <= 2.0 ** -50
         assert abs(s * s + c * c - 1.0) < 2.0 ** -51
-    for j in range(1, 9):  # sin 2a = 2 sin a cos a, cos 2a = c^2 - s^2
+    for j in range(1, 65):  # sin 2a = 2 sin a cos a, cos 2a = c^2 - s^2
         s, c = sc[j]
         assert abs(sc[2 * j][0] - 2 * s * c) < 2.0 ** -51
         assert abs(sc[2 * j][1] - (c * c - s * s)) < 2.0 ** -51
+    for j in range(65):  # symmetries: sin(pi - a) = sin a, cos(pi - a) = -cos a, and the half turn
+        assert sc[64 - j][0] == sc[j][0] and sc[64 - j][1] == -sc[j][1], j
+        assert sc[64 + j][0] == -sc[j][0] and sc[64 + j][1] == -sc[j][1], j
