@@ -398,7 +398,7 @@ def test_split_k_reduction_matches_single_pass_bound_and_repeats(M, N, K, prec):
 
 # ----------------------------------------------------- full-size sampled parity
 
-def _sampled_full_size(model, M, prec, mech, delta, eps, nsample=48):
+def _sampled_full_size(model, M, prec, mech, delta, eps, nsample=256, nrows=16):
     gm, om = MECH[mech]
     gp, op = PREC[prec]
     g = np.random.Generator(np.random.PCG64(99))
@@ -410,8 +410,9 @@ def _sampled_full_size(model, M, prec, mech, delta, eps, nsample=48):
         Wd = dev_w(W)
         C = sp.correction(Wd, M, gm, delta, eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
         Y = host(sp.masked_linear_fused(dev(X), Wd, C, gm, delta, eps, 0, sid, 0, gp))
-        rows = g.choice(M, size=min(M, 8), replace=False)
-        cols = g.choice(N, size=nsample, replace=False)
+        # the first and last row and column (the edge tiles) and random others
+        rows = np.unique(np.concatenate([[0, M - 1], g.choice(M, size=min(M, nrows - 2), replace=False)]))
+        cols = np.unique(np.concatenate([[0, N - 1], g.choice(N, size=nsample - 2, replace=False)]))
         for i in rows:
             eta = O.noise(1, K, om, delta, eps, 0, sid, int(i))
             xt = O.mask(X[i:i + 1], eta)

@@ -182,7 +182,7 @@ def test_tiled_split_k_repeats_and_matches_row_major_bound(M, N, K, prec):
     assert np.all(np.abs(rowmajor.astype(np.float64) - ref) <= bound)
 
 
-def _sampled_full_size_tiled(model, M, prec, mech, omech, delta, eps, nsample=48):
+def _sampled_full_size_tiled(model, M, prec, mech, omech, delta, eps, nsample=256, nrows=16):
     # the launch configuration of the bench: full projection shapes, tiled W,
     # outputs checked on sampled rows and columns
     gp, op = PREC[prec]
@@ -195,8 +195,9 @@ def _sampled_full_size_tiled(model, M, prec, mech, omech, delta, eps, nsample=48
         T = sp.tile_weights(dev(W).to(torch.bfloat16))
         C = sp.correction(T, M, mech, delta, eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
         Y = host(sp.masked_linear_fused(dev(X), T, C, mech, delta, eps, 0, sid, 0, gp))
-        rows = g.choice(M, size=min(M, 6), replace=False)
-        cols = g.choice(N, size=nsample, replace=False)
+        # the first and last row and column (the edge tiles) and random others
+        rows = np.unique(np.concatenate([[0, M - 1], g.choice(M, size=min(M, nrows - 2), replace=False)]))
+        cols = np.unique(np.concatenate([[0, N - 1], g.choice(N, size=nsample - 2, replace=False)]))
         for i in rows:
             eta = O.noise(1, K, omech, delta, eps, 0, sid, int(i))
             Ws = W[cols]
@@ -213,6 +214,11 @@ def test_tiled_llama_layer_sampled(M):
 @pytest.mark.parametrize("M", [1, 4, 16, 64, 1024])
 def test_tiled_qwen_layer_sampled(M):
     _sampled_full_size_tiled(WL.QWEN3_4B, M, "bf16x3", sp.SPLITEE_MECH_LAPLACE, O.MECH_LAPLACE, 719.8, 2.0)
+
+
+def test_tiled_qwen_headline_configuration_sampled():
+    # the bench's default launch configuration: 1024 tokens, Gaussian noise, Delta = eps = 1
+    _sampled_full_size_tiled(WL.QWEN3_4B, 1024, "bf16x3", sp.SPLITEE_MECH_GAUSSIAN, O.MECH_GAUSSIAN, 1.0, 1.0)
 
 
 @pytest.mark.parametrize("M", [128, 4, 64])
