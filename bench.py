@@ -100,7 +100,7 @@ WORKLOADS = ["llama3b-layer-m128", "single-fp32-m32", "llama3b-28l-m512", "qwen3
              "qwen3-4b-decode-m1", "qwen3-4b-decode-m4", "qwen3-4b-decode-m16", "qwen3-4b-decode-m64",
              "llama3b-lmhead-m1", "llama3b-lmhead-m15", "llama3b-lmhead-m128",
              "qwen3-4b-lmhead-m1", "qwen3-4b-lmhead-m15"]
-STEP_MASKS_MAX_M = 16  # up to this many tokens the masks of a step are drawn in one launch
+STEP_MASKS_MAX_M = 64  # up to this many tokens the masks of a step are drawn in one launch
 DECODE_POS = 1024  # decode position t: rows [t, t+M) of the 2048-position correction bank
 
 
@@ -133,11 +133,12 @@ class Path:
     group, the weights, the precomputed correction rows and the outputs.
 
     Prefill-sized M: per projection, noise + mask in one kernel, then the GEMM with
-    the unmask epilogue.  Up to `step_masks_max_m` tokens the noise does not fill the
-    chip one projection at a time, so one launch per step draws the masks of every
-    layer and projection group (the noise does not depend on the input), and the
-    fused call of each projection forms fl32(X + eta) from the drawn mask: inside the
-    skinny GEMM at M <= 16, by the mask kernel ahead of the streamed GEMM above."""
+    the unmask epilogue.  Up to `step_masks_max_m` tokens (64: measured faster at 64,
+    slower at 128 and 1024) the noise does not fill the chip one projection at a time, so
+    one launch per step draws the masks of every layer and projection group (the noise
+    does not depend on the input), and the fused call of each projection forms
+    fl32(X + eta) from the drawn mask inside its GEMM: the skinny kernel at M <= 16, the
+    streamed kernel's in-kernel mask above."""
 
     def __init__(self, torch, sp, WL, name, prec, mech, delta, eps, weight_sets, layout="auto",
                  step_masks_max_m=STEP_MASKS_MAX_M):

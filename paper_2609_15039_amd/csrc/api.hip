@@ -114,6 +114,13 @@ int run_masked(const float* X, int64_t ldx, const void* W, int w_type, int64_t l
         // decode with a precomputed mask: the GEMM forms fl32(X + eta) itself
         return splitee_host::launch_skinny_masked(X, ldx, eta_override, K, prec, W, w_type, ldw, C, ldc, Y, ldy, M, N,
                                                   K, base, gws, s);
+    if (eta_override) {
+        // prefill-sized M with a precomputed mask: the streamed GEMM forms fl32(X + eta)
+        // itself where its plan allows (64-row tiles), else the two launches below
+        const int rc = splitee_host::launch_gemm_masked(X, ldx, eta_override, K, prec, W, w_type, C, ldc, Y, ldy, M, N,
+                                                        K, base, gws, s);
+        if (rc != SPLITEE_ERR_UNSUPPORTED) return rc;
+    }
     void* Xt = base + gws;
     unsigned* counters = reinterpret_cast<unsigned*>(base);
     const int64_t ncounters = (int64_t)(gemm_counters(M, N, K, prec, w_type) / 4);

@@ -101,6 +101,11 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t plane_stride, cons
 int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec,
                          const void* W, int w_type, int64_t ldw, const float* C, int64_t ldc, float* Out,
                          int64_t ldo, int64_t M, int64_t N, int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
+// The streamed GEMM with its masked input formed in-kernel the same way (64-row tiles on
+// tiled W, M <= 128); SPLITEE_ERR_UNSUPPORTED where the plan has no such variant.
+int launch_gemm_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec, const void* W,
+                       int w_type, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M, int64_t N,
+                       int64_t K, void* ws, size_t ws_bytes, hipStream_t s);
 size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec, int w_type);
 int launch_skinny(const void* A, int prec, int64_t lda, int64_t plane_stride, const void* W, int w_type,
                   int64_t ldw, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M,

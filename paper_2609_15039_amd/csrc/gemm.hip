@@ -496,6 +496,220 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
                     make_float4(acc[i][j][4 * c], acc[i][j][4 * c + 1], acc[i][j][4 * c + 2], acc[i][j][4 * c + 3]);
 }
 
+// The W-streamed kernel with the masked input formed in the kernel (64-row tiles,
+// tiled W): for a mask eta drawn ahead, each thread loads 8 consecutive float32 of X
+// and of eta of one row, one K tile ahead, forms fl32(X + eta), splits it into the NPL
+// bfloat16 planes (the mask kernel's split, so the planes are the same bits) and
+// writes them into the swizzled LDS stage the buffer-load-to-LDS fills in
+// gemm_stream_kernel; W streams into registers D tiles ahead as there.  This saves
+// the separate mask launch (and its planes' round trip through memory) where the
+// masked input is read by few column tiles: up to 128 tokens.
+template <int NPL, int BM, int BN, int WGM, int D, int NW>
+__global__ void __launch_bounds__(NW * WAVE)
+gemm_stream_masked_kernel(const float* __restrict__ X, int64_t ldx, const float* __restrict__ E, int64_t lde,
+                          const uint16_t* __restrict__ W, const float* __restrict__ C, int64_t ldc,
+                          float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
+                          int ksplit, int kt_per_split, float* __restrict__ part)
+{
+    constexpr int WGN = NW / WGM;
+    constexpr int WTM = BM / WGM, WTN = BN / WGN;
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int S = D + 1;
+    constexpr int SB = NPL * BM * 128;        // LDS bytes per stage
+    constexpr int LW = 4 * TN;                // W loads per wave per tile
+    static_assert(WGM * WGN == NW && TM * 32 * WGM == BM && TN * 32 * WGN == BN, "wave tile");
+    static_assert(BM * 8 == NW * WAVE, "one 8-element unit of the masked input per thread");
+    static_assert(S >= 3 && S <= 4 && (D - 1) * LW + 4 < 64, "stages");
+
+    const int tid = threadIdx.x, lane = tid % WAVE;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / WAVE);
+    const int wm = wave / WGN, wn = wave % WGN;
+    const uint32_t lb = splitee::xcd_logical_block(blockIdx.x, gridDim.x);
+    const int tiles = mtiles * ntiles;
+    const int split = (int)lb / tiles, tile = (int)lb % tiles;
+    const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
+    const int ktiles = (K + BK - 1) / BK;
+    const int kt0 = split * kt_per_split;
+    const int kt1 = min(kt0 + kt_per_split, ktiles);
+    const int nk = kt1 > kt0 ? kt1 - kt0 : 0;
+    const int nloop = (nk + S - 1) / S * S;
+
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, (uint32_t)((int64_t)M * ldx * 4));
+    const __amdgpu_buffer_rsrc_t re = make_rsrc(E, (uint32_t)((int64_t)M * lde * 4));
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)((N + 31) / 32) * ktiles * 4096));
+
+    // this thread's unit: row ur of the tile, 8 k from 8 uc of every K tile
+    const int ur = tid >> 3, uc = tid & 7;
+    const int gm = m0 + ur;
+    const uint32_t xoff = gm < M ? (uint32_t)(((int64_t)gm * ldx + uc * 8) * 4) : OOB;
+    const uint32_t eoff = gm < M ? (uint32_t)(((int64_t)gm * lde + uc * 8) * 4) : OOB;
+    const int wslot = (uc ^ lds_swizzle<1>(ur)) << 4; // the unit's 16-byte slot in each plane row
+    const int fc = lane % 32, fh = lane / 32;
+    uint32_t woff[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int gn = n0 + wn * WTN + j * 32 + fc;
+        woff[j] = gn < N ? (uint32_t)((int64_t)(gn / 32) * ktiles * 4096 + lane * 16) : OOB;
+    }
+
+    unsigned char* const st0 = stream_stage<0, SB>();
+    unsigned char* const st1 = stream_stage<1, SB>();
+    unsigned char* const st2 = stream_stage<2, SB>();
+    unsigned char* const st3 = S > 3 ? stream_stage<3, SB>() : st0;
+    auto stage = [&](auto sc) -> unsigned char* {
+        constexpr int q = decltype(sc)::value;
+        return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3;
+    };
+
+    uint4 xr[2], er[2];
+    auto load_x = [&](int t) { // X and eta of relative tile t into registers (zeros past K or M)
+        const int kt = kt0 + t, kb = kt * BK;
+        const bool ok = kt < kt1 && kb + uc * 8 < K;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            xr[h] = load16(rx, ok && xoff != OOB ? xoff + (uint32_t)(kb * 4 + 16 * h) : OOB);
+            er[h] = load16(re, ok && eoff != OOB ? eoff + (uint32_t)(kb * 4 + 16 * h) : OOB);
+        }
+    };
+    auto write_x = [&](auto sc) { // fl32(X + eta), split, into the stage's plane rows
+        unsigned char* sb = stage(sc);
+        float x[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const float4 a = __builtin_bit_cast(float4, xr[h]), b = __builtin_bit_cast(float4, er[h]);
+            x[4 * h + 0] = a.x + b.x;
+            x[4 * h + 1] = a.y + b.y;
+            x[4 * h + 2] = a.z + b.z;
+            x[4 * h + 3] = a.w + b.w;
+        }
+        uint4 q[NPL];
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            if (NPL == 1) {
+                reinterpret_cast<uint32_t*>(&q[0])[h] = splitee::bf16x2_rne(x[2 * h], x[2 * h + 1]);
+            } else {
+                splitee::split3_bf16x2(x[2 * h], x[2 * h + 1], reinterpret_cast<uint32_t*>(&q[0])[h],
+                                       reinterpret_cast<uint32_t*>(&q[1])[h], reinterpret_cast<uint32_t*>(&q[2])[h]);
+            }
+        }
+#pragma unroll
+        for (int p = 0; p < NPL; ++p)
+            *reinterpret_cast<uint4*>(sb + (p * BM + ur) * 128 + wslot) = q[p];
+    };
+
+    uint4 wb[S][TN][4];
+    auto issue_w = [&](int t, auto sc, int part) {
+        constexpr int q = decltype(sc)::value;
+        const int kt = kt0 + t;
+        const bool live = kt < kt1;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const bool ok = live && woff[j] != OOB;
+            wb[q][j][part] = load16(rw, ok ? woff[j] + (uint32_t)(kt * 4 + part) * 1024 : OOB);
+        }
+    };
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+    auto read_a = [&](const unsigned char* sb, int s, bf16x8_t (&a)[NPL][TM]) {
+        const int kc = s * 2 + fh;
+#pragma unroll
+        for (int p = 0; p < NPL; ++p)
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = p * BM + wm * WTM + i * 32 + fc;
+                a[p][i] = as_bf16x8(*reinterpret_cast<const uint4*>(sb + r * 128 + ((kc ^ lds_swizzle<1>(r)) << 4)));
+            }
+    };
+    // step t: barrier (tile t's stage, written at the end of step t - 1, is complete
+    // everywhere, and stage t - 1 is no longer read), multiply tile t from W slot t while
+    // W of tile t + D is issued, then the masked input of tile t + 1 (its X and eta loaded
+    // at the end of step t - 1) goes into its stage and the X and eta of tile t + 2 are
+    // issued.  Loads complete in order: at that wait only W of tile t + D is younger than
+    // tile t + 1's X and eta.  Stage t + 1 was last read at step t + 1 - S <= t - 2, which
+    // every wave finished before this step's barrier.
+    auto step = [&](int t, auto sc) {
+        constexpr int q = decltype(sc)::value;
+        __builtin_amdgcn_s_barrier();
+        const unsigned char* sb = stage(sc);
+        bf16x8_t a[2][NPL][TM];
+        read_a(sb, 0, a[0]);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (s + 1 < 4) read_a(sb, s + 1, a[(s + 1) & 1]);
+            issue_w(t + D, std::integral_constant<int, (q + D) % S>{}, s);
+#pragma unroll
+            for (int p = 0; p < NPL; ++p)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][p][i], as_bf16x8(wb[q][j][s]), acc[i][j], 0, 0, 0);
+        }
+        wait_vmem<LW>();
+        write_x(std::integral_constant<int, (q + 1) % S>{});
+        load_x(t + 2);
+        __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14)); // lgkmcnt(0): this wave's LDS writes done
+    };
+
+    // prologue: tile 0's masked input into stage 0, W of tiles 0 .. D - 1 and tile 1's X
+    // and eta issued, W of tile 0 landed (the younger loads may be in flight)
+    load_x(0);
+#pragma unroll
+    for (int part = 0; part < 4; ++part) issue_w(0, std::integral_constant<int, 0>{}, part);
+    wait_vmem<LW>();
+    write_x(std::integral_constant<int, 0>{});
+#pragma unroll
+    for (int part = 0; part < 4; ++part) issue_w(1, std::integral_constant<int, 1>{}, part);
+    if constexpr (D > 2) {
+#pragma unroll
+        for (int part = 0; part < 4; ++part) issue_w(2, std::integral_constant<int, 2>{}, part);
+    }
+    load_x(1);
+    wait_vmem<(D - 1) * LW + 4>();
+    __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
+    for (int t = 0; t < nloop; t += S) {
+        step(t, std::integral_constant<int, 0>{});
+        step(t + 1, std::integral_constant<int, 1>{});
+        step(t + 2, std::integral_constant<int, 2>{});
+        if constexpr (S > 3) step(t + 3, std::integral_constant<int, 3>{});
+    }
+    wait_vmem<0>();
+
+    if (ksplit == 1) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = n0 + wn * WTN + j * 32 + fc;
+                if (col >= N) continue;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = m0 + wm * WTM + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
+                    if (row < M) {
+                        float v = acc[i][j][e];
+                        if (C) v = v - C[(int64_t)row * ldc + col];
+                        Out[(int64_t)row * ldo + col] = v;
+                    }
+                }
+            }
+        return;
+    }
+    float4* mp = reinterpret_cast<float4*>(part) + (((int64_t)tile * ksplit + split) * NW + wave) * (TM * TN * 4 * 64);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                mp[((i * TN + j) * 4 + c) * 64 + lane] =
+                    make_float4(acc[i][j][4 * c], acc[i][j][4 * c + 1], acc[i][j][4 * c + 2], acc[i][j][4 * c + 3]);
+}
+
 // Sums the split-K partials of gemm_stream_kernel in split order and applies the
 // unmask epilogue.  Thread u handles one float4 of one wave's partial (the
 // register order the partials were written in): rows 8 c + 4 (l / 32) + 0..3 of
@@ -1887,6 +2101,49 @@ int launch_skinny_masked(const float* X, int64_t ldx, const float* eta, int64_t 
         return tiled ? run_gemv_tiled<true>(src, prec, W, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s)
                      : launch_gemv<true>(src, prec, W, ldw, C, ldc, Out, ldo, M, N, K, s);
     return run_skinny<true>(src, prec, W, tiled, ldw, C, ldc, Out, ldo, M, N, K, ws, ws_bytes, s);
+}
+
+// The streamed GEMM with the masked input formed in-kernel from X and a given mask eta
+// (both M x K float32), for the plans with 64-row tiles on tiled W (M <= 128);
+// SPLITEE_ERR_UNSUPPORTED for any other plan, which the caller then runs as the mask
+// launch followed by launch_gemm.
+int launch_gemm_masked(const float* X, int64_t ldx, const float* eta, int64_t ld_eta, int prec, const void* W,
+                       int w_type, const float* C, int64_t ldc, float* Out, int64_t ldo, int64_t M, int64_t N,
+                       int64_t K, void* ws, size_t ws_bytes, hipStream_t s)
+{
+    if (M == 0 || N == 0) return SPLITEE_OK;
+    if (prec == SPLITEE_PREC_F32 || w_type != SPLITEE_BF16_TILED || M > 128) return SPLITEE_ERR_UNSUPPORTED;
+    if (!X || !eta) return SPLITEE_ERR_ARG;
+    if (K % 8 != 0 || ld_eta < K || ldx < K) return SPLITEE_ERR_SHAPE;
+    if (M * ld_eta * 4 >= (int64_t(1) << 31) || M * ldx * 4 >= (int64_t(1) << 31) ||
+        (int64_t)splitee::tiled_weights_bytes(N, K) >= (int64_t(1) << 31))
+        return SPLITEE_ERR_UNSUPPORTED;
+    const bool allow_split = ws != nullptr;
+    Plan p = plan_tiled(M, N, K, prec, w_type, allow_split);
+    if (p.variant != 24 && p.variant != 25 && p.variant != 26 && p.variant != 27) return SPLITEE_ERR_UNSUPPORTED;
+    if (p.ksplit > 1 && ws_bytes < p.counter_bytes + p.part_bytes) return SPLITEE_ERR_WORKSPACE;
+    float* pp = reinterpret_cast<float*>(ws);
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
+    dim3 grid((unsigned)(p.mtiles * p.ntiles * p.ksplit));
+    const int m = (int)M, n = (int)N, k = (int)K;
+#define SM_LAUNCH(NP, BM_, BN_, WGM_, D_) hipLaunchKernelGGL((gemm_stream_masked_kernel<NP, BM_, BN_, WGM_, D_, 8>), grid, dim3(8 * WAVE), 0, s, X, ldx, eta, ld_eta, w, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
+    switch (p.variant) {
+    case 24: SM_LAUNCH(3, 64, 256, 1, 2); break;
+    case 25: SM_LAUNCH(1, 64, 256, 1, 2); break;
+    case 26: SM_LAUNCH(3, 64, 128, 2, 3); break;
+    default: SM_LAUNCH(1, 64, 128, 2, 3); break;
+    }
+#undef SM_LAUNCH
+    if (p.ksplit > 1) {
+        const int tiles = p.mtiles * p.ntiles;
+        const int64_t units = (int64_t)tiles * p.bm * p.bn / 4;
+        const dim3 g2((unsigned)((units + 255) / 256));
+        if (p.variant == 24 || p.variant == 25)
+            hipLaunchKernelGGL((stream_sum_kernel<64, 256, 1, 8>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
+        else
+            hipLaunchKernelGGL((stream_sum_kernel<64, 128, 2, 4>), g2, dim3(256), 0, s, pp, p.ksplit, C, ldc, Out, ldo, m, n, p.mtiles, tiles);
+    }
+    return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
 
 }  // namespace splitee_host

@@ -136,11 +136,12 @@ def test_tiled_exact_cancellation_integer_mask(prec, M):
 
 
 @pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
-@pytest.mark.parametrize("M", [1, 2, 3, 16])
+@pytest.mark.parametrize("M", [1, 2, 3, 16, 17, 64, 100, 128])
 @pytest.mark.parametrize("N,K", [(6144, 2560), (200, 9728), (40, 264)])
 def test_tiled_precomputed_mask_is_the_two_launch_path(prec, M, N, K):
-    # the decode kernel forms fl32(X + eta) itself: bit for bit the mask kernel
-    # followed by the GEMM, on tiled W
+    # the decode kernels (M <= 16) and the streamed kernel with 64-row tiles (M <= 128)
+    # form fl32(X + eta) themselves: bit for bit the mask kernel followed by the GEMM, on
+    # tiled W
     gp, op = PREC[prec]
     gm = sp.SPLITEE_MECH_GAUSSIAN
     sid, row0 = WL.stream_id(2, 1), 500 + M
@@ -156,6 +157,24 @@ def test_tiled_precomputed_mask_is_the_two_launch_path(prec, M, N, K):
     eta_o = O.noise(M, K, O.MECH_GAUSSIAN, 719.8, 2.0, 0, sid, row0)
     b = O.error_bounds(X, eta_o, O.mask(X, eta_o), W, op)
     assert np.all(np.abs(Y.astype(np.float64) - O.gemm64(X, W)) <= b["gate"])
+
+
+@pytest.mark.parametrize("prec", ["bf16", "bf16x3"])
+@pytest.mark.parametrize("M", [64, 128])
+def test_tiled_precomputed_mask_wide_n_is_the_two_launch_path(prec, M):
+    # the 64 x 256 tiles of the in-kernel mask (gate/up widths), split over K
+    gp, _ = PREC[prec]
+    gm = sp.SPLITEE_MECH_GAUSSIAN
+    N, K = 19456, 2560
+    sid, row0 = WL.stream_id(4, 2), 300
+    X = WL.gen_x(M, K, seed=33)
+    T = sp.tile_weights(dev(WL.gen_w(N, K, seed=34)).to(torch.bfloat16))
+    Xd = dev(X)
+    eta = sp.noise(M, K, gm, 719.8, 2.0, 0, sid, row0=row0)
+    C = sp.correction(T, M, gm, 719.8, 2.0, 0, sid, row0, sp.SPLITEE_PREC_BF16X3)
+    Y = host(sp.masked_linear_fused(Xd, T, C, gm, 719.8, 2.0, 0, sid, row0, gp, eta_override=eta))
+    Y2 = host(sp.masked_linear_unmask(sp.mask(Xd, eta, gp), gp, T, C))
+    assert np.array_equal(bits(Y), bits(Y2))
 
 
 @pytest.mark.parametrize("M,N,K,prec", [(128, 16384, 3072, "bf16x3"), (128, 5120, 3072, "bf16x3"),
