@@ -252,7 +252,9 @@ size_t splitee_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, int prec);
  * vector-ALU GEMV, on whole rows of row-major W or 32-row blocks of tiled W; else
  * the skinny MFMA kernel); given eta_override they form fl32(X + eta) and its
  * bfloat16 planes themselves (one launch, bit-identical to the two-launch path).  Otherwise the tiled
- * or W-streamed MFMA kernel runs, split over K when the tile count is small.
+ * or W-streamed MFMA kernel runs, split over K when the tile count is small; for
+ * 17 <= M <= 128 on tiled W given eta_override, the streamed kernel too forms the masked
+ * input itself (bit-identical to the mask launch followed by the GEMM).
  * workspace: >= splitee_fused_workspace_bytes(M, N, K, prec) bytes, 256-byte
  * aligned; it must hold zeros before its first use and calls leave it that way.
  */
