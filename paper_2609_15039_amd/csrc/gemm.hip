@@ -498,10 +498,11 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
 
 // The W-streamed kernel with the masked input formed in the kernel (64-row tiles,
 // tiled W): for a mask eta drawn ahead, each thread loads 8 consecutive float32 of X
-// and of eta of one row, one K tile ahead, forms fl32(X + eta), splits it into the NPL
-// bfloat16 planes (the mask kernel's split, so the planes are the same bits) and
-// writes them into the swizzled LDS stage the buffer-load-to-LDS fills in
-// gemm_stream_kernel; W streams into registers D tiles ahead as there.  This saves
+// and of eta of one row two K tiles ahead and, after the current tile's MFMAs, forms
+// the next tile's fl32(X + eta), splits it into the NPL bfloat16 planes (the mask
+// kernel's split, so the planes are the same bits) and writes them into the swizzled
+// LDS stage the buffer-load-to-LDS fills in gemm_stream_kernel; W streams into
+// registers D tiles ahead as there.  This saves
 // the separate mask launch (and its planes' round trip through memory) where the
 // masked input is read by few column tiles: up to 128 tokens.
 template <int NPL, int BM, int BN, int WGM, int D, int NW>
