@@ -927,7 +927,12 @@ struct SkSrc {
     const float* eta; int64_t ld_eta;
 };
 
-constexpr int SK_MCP = 2; // masked-input units (8 float32 of X and of eta) per thread per load round
+// Masked-input units (8 float32 of X and of eta) per thread per load round of the skinny
+// kernel when it forms the mask: 2 up to 8 rows, 4 above, so that at 16 rows and 16 k steps
+// per split the whole slice is requested before the W ring (a round issued after the ring
+// waits for all of it, since a wave's loads complete in order).  Measured on the Qwen3-4B
+// projections: 4 per round made 16 rows 4.8% faster and 4 rows 3.7% slower.
+constexpr int SK_MCP_SMALL = 2, SK_MCP_LARGE = 4;
 
 template <int NPL>
 __device__ __forceinline__ void planes_of(const float (&x)[8], uint4 (&q)[NPL])
@@ -943,7 +948,7 @@ __device__ __forceinline__ void planes_of(const float (&x)[8], uint4 (&q)[NPL])
     }
 }
 
-template <int NPL, int R, bool MASK, bool TILED = false>
+template <int NPL, int R, bool MASK, bool TILED = false, int MCP = SK_MCP_SMALL>
 __global__ void __launch_bounds__(256)
 skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
               float* __restrict__ Out, int64_t ldo, int M, int N, int K, int ntiles, int ksplit,
@@ -1022,9 +1027,9 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
             k = s0 * 32 + c * 8;
             return u < units && c < ns * 4 && k < K;
         };
-        auto round_load = [&](int base, uint4 (&xv)[SK_MCP][2], uint4 (&ev)[SK_MCP][2]) {
+        auto round_load = [&](int base, uint4 (&xv)[MCP][2], uint4 (&ev)[MCP][2]) {
 #pragma unroll
-            for (int i = 0; i < SK_MCP; ++i) {
+            for (int i = 0; i < MCP; ++i) {
                 int r, c, k;
                 const bool ok = unit_ok(base + i * 256 + tid, r, c, k);
                 const uint32_t ox = ok ? (uint32_t)(((int64_t)r * src.ldx + k) * 4) : OOB;
@@ -1036,9 +1041,9 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
                 }
             }
         };
-        auto round_store = [&](int base, const uint4 (&xv)[SK_MCP][2], const uint4 (&ev)[SK_MCP][2]) {
+        auto round_store = [&](int base, const uint4 (&xv)[MCP][2], const uint4 (&ev)[MCP][2]) {
 #pragma unroll
-            for (int i = 0; i < SK_MCP; ++i) {
+            for (int i = 0; i < MCP; ++i) {
                 const int u = base + i * 256 + tid;
                 if (u < units) {
                     const int r = u / upr, c = u - r * upr;
@@ -1060,12 +1065,12 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
                 }
             }
         };
-        uint4 xv[SK_MCP][2], ev[SK_MCP][2];
+        uint4 xv[MCP][2], ev[MCP][2];
         round_load(0, xv, ev);
 #pragma unroll
         for (int u = 0; u < R; ++u) ring[u] = wload(u);
         round_store(0, xv, ev);
-        for (int base = SK_MCP * 256; base < units; base += SK_MCP * 256) {
+        for (int base = MCP * 256; base < units; base += MCP * 256) {
             round_load(base, xv, ev);
             round_store(base, xv, ev);
         }
@@ -2040,9 +2045,18 @@ int run_skinny(const SkSrc& src, int prec, const void* W, bool tiled, int64_t ld
     float* part = p.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.counter_bytes) : nullptr;
     dim3 grid((unsigned)(p.ntiles * p.ksplit));
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
-#define SK_LAUNCH(NP, T) hipLaunchKernelGGL((skinny_kernel<NP, SK_RING, MASK, T>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters)
-    if (npl == 1) { if (tiled) SK_LAUNCH(1, true); else SK_LAUNCH(1, false); }
-    else { if (tiled) SK_LAUNCH(3, true); else SK_LAUNCH(3, false); }
+#define SK_LAUNCH(NP, T, MC) hipLaunchKernelGGL((skinny_kernel<NP, SK_RING, MASK, T, MC>), grid, dim3(256), lds, s, src, w, ldw, C, ldc, Out, ldo, (int)M, (int)N, (int)K, p.ntiles, p.ksplit, p.kt_per_split, part, counters)
+#define SK_LAUNCH_MC(NP, T)                                                                  \
+    do {                                                                                     \
+        if constexpr (MASK) {                                                                \
+            if (M > 8) SK_LAUNCH(NP, T, SK_MCP_LARGE); else SK_LAUNCH(NP, T, SK_MCP_SMALL); \
+        } else {                                                                             \
+            SK_LAUNCH(NP, T, SK_MCP_SMALL);                                                  \
+        }                                                                                    \
+    } while (0)
+    if (npl == 1) { if (tiled) SK_LAUNCH_MC(1, true); else SK_LAUNCH_MC(1, false); }
+    else { if (tiled) SK_LAUNCH_MC(3, true); else SK_LAUNCH_MC(3, false); }
+#undef SK_LAUNCH_MC
 #undef SK_LAUNCH
     return hipGetLastError() == hipSuccess ? SPLITEE_OK : SPLITEE_ERR_HIP;
 }
