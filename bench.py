@@ -482,14 +482,14 @@ def weight_tiled(layout, M, N, K):
     """Whether a bfloat16 projection of N output rows and K columns at M tokens stores W
     tiled.  auto: one or two tokens run a vector-ALU GEMV, on row-major W (whole rows per
     wave) or on tiled W (32-row blocks); measured on the Llama-3.2-3B and Qwen3-4B
-    projections and on 2560-24576 x 2560-4096 matrices, the tiled one is faster from 8192
-    rows up at one token (8192 x 3072: 12.9 -> 12.1 us, Llama-3.2-3B gate/up 21.9 -> 19.4 us;
-    at 6144 rows a tie) and from about 12 M elements up at two (Qwen3-4B Down 20.2 -> 15.3 us),
-    the row-major one below (Qwen3-4B O at one token 7.1 us against 9.0); every other M runs
-    the MFMA kernels on tiled W."""
+    projections and on 2560-24576 x 2560-4096 matrices, the tiled one is faster from 6144
+    rows up at one token (Qwen3-4B QKV 9.6 -> 9.0 us, 6144 x 3072 10.8 -> 10.4 us, Llama-3.2-3B
+    gate/up 21.9 -> 19.4 us; 5120 rows 9.3 against 9.8) and from about 12 M elements up at two
+    (Qwen3-4B Down 20.2 -> 15.1 us), the row-major one below (Qwen3-4B O at one token 7.0 us
+    against 8.9); every other M runs the MFMA kernels on tiled W."""
     if layout == "auto":
         if M == 1:
-            return N >= 8192
+            return N >= 6144
         if M == 2:
             return N * K >= 12 * 2**20
         return True
