@@ -1347,9 +1347,9 @@ gemv_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const float*
 // GEMV with K split over the waves (K <= 16384 and fewer than GS_MAX_PAIRS row pairs;
 // the kernel above serves longer rows and the widest N).
 // A workgroup owns GS_ROWS (4 or 5) W rows; wave w takes the 512-k chunks j = w, w + 4, ..
-// of each row, issues all of its W loads at once, forms
-// the masked input of its own chunks in registers (from X + eta or from the
-// planes, exactly as above), accumulates fma(x~, w, acc) in chunk and k order,
+// of each row, issues the loads of its chunks' masked input and then all of its W loads
+// at once, forms the masked input in registers (from X + eta or from the planes,
+// exactly as above) while W is in flight, accumulates fma(x~, w, acc) in chunk and k order,
 // sums its lanes with the same butterfly, and the four waves' sums are added in
 // wave order.
 constexpr int GS_MAX_CH = 8;  // chunks per wave: K <= 4 x 8 x 512
@@ -1367,18 +1367,10 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
     const int nchunk = (K + 511) / 512;
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
 
-    uint4 wv[CH][GS_ROWS];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        const int j = wave + GV_WAVES * c, k = 512 * j + 8 * lane;
-#pragma unroll
-        for (int r = 0; r < GS_ROWS; ++r) {
-            const bool ok = j < nchunk && k < K && n0 + r < N;
-            wv[c][r] = load16(rw, ok ? (uint32_t)(((int64_t)(n0 + r) * ldw + k) * 2) : OOB);
-        }
-    }
-    // the masked input of the wave's chunks, through buffer resources so that the
-    // loads are unconditional (past K they read zeros)
+    // the masked input of the wave's chunks first, through buffer resources so that the
+    // loads are unconditional (past K they read zeros): a wave's loads complete in order,
+    // so loads issued after W's would hold the conversion until all of W has landed (two
+    // tokens 13% faster on the Qwen3-4B and Llama-3.2-3B projections with this order)
     const int MRr = MR;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(MASK ? (const void*)src.X : (const void*)src.A,
                                                 MASK ? (uint32_t)((int64_t)MRr * src.ldx * 4)
@@ -1425,6 +1417,17 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
         }
     }
 
+    // then every W load of the wave, all in flight at once
+    uint4 wv[CH][GS_ROWS];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int j = wave + GV_WAVES * c, k = 512 * j + 8 * lane;
+#pragma unroll
+        for (int r = 0; r < GS_ROWS; ++r) {
+            const bool ok = j < nchunk && k < K && n0 + r < N;
+            wv[c][r] = load16(rw, ok ? (uint32_t)(((int64_t)(n0 + r) * ldw + k) * 2) : OOB);
+        }
+    }
     float acc[MR][GS_ROWS];
 #pragma unroll
     for (int m = 0; m < MR; ++m)
