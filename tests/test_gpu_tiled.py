@@ -240,6 +240,32 @@ def test_tiled_qwen_headline_configuration_sampled():
     _sampled_full_size_tiled(WL.QWEN3_4B, 1024, "bf16x3", sp.SPLITEE_MECH_GAUSSIAN, O.MECH_GAUSSIAN, 1.0, 1.0)
 
 
+@pytest.mark.parametrize("model,M", [("qwen", 1024), ("llama", 512), ("llama", 128), ("qwen", 64), ("qwen", 16),
+                                     ("qwen", 4), ("qwen", 1)])
+@pytest.mark.parametrize("mech,omech,delta,eps", [(sp.SPLITEE_MECH_GAUSSIAN, O.MECH_GAUSSIAN, 1.0, 1.0),
+                                                   (sp.SPLITEE_MECH_LAPLACE, O.MECH_LAPLACE, 719.8, 2.0)])
+def test_tiled_full_size_every_element(model, M, mech, omech, delta, eps):
+    # the bench's workloads at full size in its launch configuration (one layer of the model,
+    # tiled W, bf16x3): every output element of every projection against its Theorem-4 gate
+    gp, op = PREC["bf16x3"]
+    shape = WL.QWEN3_4B if model == "qwen" else WL.LLAMA_3B
+    for proj in shape.projections():
+        K, N = proj.K, proj.N
+        sid = WL.stream_id(0, proj.group)
+        X = WL.gen_x(M, K, seed=1)
+        W = WL.gen_w(N, K, seed=2)
+        T = sp.tile_weights(dev(W).to(torch.bfloat16))
+        C = sp.correction(T, M, mech, delta, eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
+        Y = host(sp.masked_linear_fused(dev(X), T, C, mech, delta, eps, 0, sid, 0, gp)).astype(np.float64)
+        del T, C
+        eta = O.noise(M, K, omech, delta, eps, 0, sid, 0)
+        gate = O.error_bounds(X, eta, O.mask(X, eta), W, op)["gate"]
+        err = np.abs(Y - O.gemm64(X, W))
+        bad = int((err > gate).sum())
+        assert bad == 0, "%s: %d of %d elements above the gate (max err/gate %.3g)" % (
+            proj.name, bad, err.size, float((err / gate).max()))
+
+
 @pytest.mark.parametrize("M", [128, 4, 64])
 def test_tiled_graph_replay_matches_eager(M):
     # noise + mask and GEMM + unmask on tiled W captured in a HIP graph: every replay,
