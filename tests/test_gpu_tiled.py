@@ -240,13 +240,16 @@ def test_tiled_qwen_headline_configuration_sampled():
     _sampled_full_size_tiled(WL.QWEN3_4B, 1024, "bf16x3", sp.SPLITEE_MECH_GAUSSIAN, O.MECH_GAUSSIAN, 1.0, 1.0)
 
 
-@pytest.mark.parametrize("model,M", [("qwen", 1024), ("llama", 512), ("llama", 128), ("qwen", 64), ("qwen", 16),
-                                     ("qwen", 4), ("qwen", 1)])
+@pytest.mark.parametrize("model,M,layout", [("qwen", 1024, "tiled"), ("llama", 512, "tiled"), ("llama", 128, "tiled"),
+                                            ("qwen", 64, "tiled"), ("qwen", 16, "tiled"), ("qwen", 4, "tiled"),
+                                            ("qwen", 2, "tiled"), ("qwen", 2, "row"), ("qwen", 1, "tiled"),
+                                            ("qwen", 1, "row")])
 @pytest.mark.parametrize("mech,omech,delta,eps", [(sp.SPLITEE_MECH_GAUSSIAN, O.MECH_GAUSSIAN, 1.0, 1.0),
                                                    (sp.SPLITEE_MECH_LAPLACE, O.MECH_LAPLACE, 719.8, 2.0)])
-def test_tiled_full_size_every_element(model, M, mech, omech, delta, eps):
+def test_tiled_full_size_every_element(model, M, layout, mech, omech, delta, eps):
     # the bench's workloads at full size in its launch configuration (one layer of the model,
-    # tiled W, bf16x3): every output element of every projection against its Theorem-4 gate
+    # bf16x3; tiled W, and at one and two tokens also the row-major W of the decode GEMV):
+    # every output element of every projection against its Theorem-4 gate
     gp, op = PREC["bf16x3"]
     shape = WL.QWEN3_4B if model == "qwen" else WL.LLAMA_3B
     for proj in shape.projections():
@@ -254,7 +257,7 @@ def test_tiled_full_size_every_element(model, M, mech, omech, delta, eps):
         sid = WL.stream_id(0, proj.group)
         X = WL.gen_x(M, K, seed=1)
         W = WL.gen_w(N, K, seed=2)
-        T = sp.tile_weights(dev(W).to(torch.bfloat16))
+        T = sp.tile_weights(dev(W).to(torch.bfloat16)) if layout == "tiled" else dev(W).to(torch.bfloat16)
         C = sp.correction(T, M, mech, delta, eps, 0, sid, 0, sp.SPLITEE_PREC_BF16X3)
         Y = host(sp.masked_linear_fused(dev(X), T, C, mech, delta, eps, 0, sid, 0, gp)).astype(np.float64)
         del T, C
