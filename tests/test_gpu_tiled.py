@@ -269,6 +269,31 @@ def test_tiled_full_size_every_element(model, M, layout, mech, omech, delta, eps
             proj.name, bad, err.size, float((err / gate).max()))
 
 
+@pytest.mark.parametrize("prec,layout", [("bf16", "tiled"), ("f32", "row")])
+@pytest.mark.parametrize("M", [1024, 64])
+def test_full_size_every_element_other_modes(prec, layout, M):
+    # the bench's other precision modes at the headline shapes (one Qwen3-4B layer): single-pass
+    # bfloat16 on tiled W, and the binary32 MFMA path on row-major bfloat16 W; every element
+    gp, op = {"bf16": (sp.SPLITEE_PREC_BF16, O.PREC_BF16), "f32": (sp.SPLITEE_PREC_F32, O.PREC_F32)}[prec]
+    for proj in WL.QWEN3_4B.projections():
+        K, N = proj.K, proj.N
+        sid = WL.stream_id(0, proj.group)
+        X = WL.gen_x(M, K, seed=1)
+        W = WL.gen_w(N, K, seed=2)
+        Wd = dev(W).to(torch.bfloat16)
+        T = sp.tile_weights(Wd) if layout == "tiled" else Wd
+        cprec = sp.SPLITEE_PREC_F32 if prec == "f32" else sp.SPLITEE_PREC_BF16X3
+        C = sp.correction(T, M, sp.SPLITEE_MECH_GAUSSIAN, 1.0, 1.0, 0, sid, 0, cprec)
+        Y = host(sp.masked_linear_fused(dev(X), T, C, sp.SPLITEE_MECH_GAUSSIAN, 1.0, 1.0, 0, sid, 0, gp))
+        del T, C, Wd
+        eta = O.noise(M, K, O.MECH_GAUSSIAN, 1.0, 1.0, 0, sid, 0)
+        gate = O.error_bounds(X, eta, O.mask(X, eta), W, op)["gate"]
+        err = np.abs(Y.astype(np.float64) - O.gemm64(X, W))
+        bad = int((err > gate).sum())
+        assert bad == 0, "%s %s: %d of %d elements above the gate (max err/gate %.3g)" % (
+            prec, proj.name, bad, err.size, float((err / gate).max()))
+
+
 @pytest.mark.parametrize("M", [128, 4, 64])
 def test_tiled_graph_replay_matches_eager(M):
     # noise + mask and GEMM + unmask on tiled W captured in a HIP graph: every replay,
