@@ -1798,6 +1798,9 @@ Plan plan_skinny(int64_t M, int64_t N, int64_t K, int prec)
     if (ks < 1) ks = 1;
     int sps = p.ktiles > 0 ? (p.ktiles + ks - 1) / ks : 1;
     while (sps > 1 && skinny_lds_bytes(M > 0 ? M : 1, npl, sps) > (size_t)SK_LDS_MAX) --sps;
+    // the same number of splits, evened out (an LDS-limited split count can leave a short
+    // last split: the Llama-3.2-3B LM head at 4 tokens, 96 steps, took 80 + 16)
+    if (p.ktiles > 0) sps = (p.ktiles + (p.ktiles + sps - 1) / sps - 1) / ((p.ktiles + sps - 1) / sps);
     p.kt_per_split = sps;
     p.ksplit = p.ktiles > 0 ? (p.ktiles + sps - 1) / sps : 1;
     p.counter_bytes = p.ksplit > 1 ? (((size_t)p.ntiles * 4 + 255) / 256) * 256 : 0;
