@@ -292,6 +292,47 @@ __device__ __forceinline__ int lds_swizzle(int r)
     return SW == 0 ? (r & 7) : ((r >> 1) & 7);
 }
 
+// Unmask epilogue of an unsplit wave tile held in v_mfma_f32_32x32x16 accumulators
+// (TM x TN blocks, rows r0 + 32 i + 8 (e / 4) + 4 h + e % 4, columns c0 + 32 j + c for
+// lane (c, h)): Out = acc - C.  Every C load of the tile is issued before the first
+// subtraction, so the wave waits for them once; loading and storing element by element
+// made each load a separate round trip (64 per lane, about 30 us per workgroup while the
+// other workgroups of the CU streamed their operands).  Elements outside M x N load C[0]
+// (always valid: the kernels run only for M, N >= 1) and store nothing.
+template <int TM, int TN>
+__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], const float* __restrict__ C, int64_t ldc,
+                                           float* __restrict__ Out, int64_t ldo, int M, int N, int r0, int c0,
+                                           int fc, int fh)
+{
+    float cv[TM][TN][16];
+    if (C) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = c0 + j * 32 + fc;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = r0 + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
+                    const bool ok = row < M && col < N;
+                    cv[i][j][e] = C[ok ? (int64_t)row * ldc + col : 0];
+                }
+            }
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = c0 + j * 32 + fc;
+            if (col >= N) continue;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = r0 + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
+                if (row < M) Out[(int64_t)row * ldo + col] = C ? acc[i][j][e] - cv[i][j][e] : acc[i][j][e];
+            }
+        }
+}
+
 template <int NPL, int BM, int BN, int WGM, int D, int NW = ST_NW, bool TILED = false, int SW = 1>
 __global__ void __launch_bounds__(NW * WAVE)
 gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
@@ -466,22 +507,7 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     wait_vmem<0>(); // the ring's last (zero) tiles have landed before the workgroup ends
 
     if (ksplit == 1) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int col = n0 + wn * WTN + j * 32 + fc;
-                if (col >= N) continue;
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int row = m0 + wm * WTM + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
-                    if (row < M) {
-                        float v = acc[i][j][e];
-                        if (C) v = v - C[(int64_t)row * ldc + col];
-                        Out[(int64_t)row * ldo + col] = v;
-                    }
-                }
-            }
+        store_tile<TM, TN>(acc, C, ldc, Out, ldo, M, N, m0 + wm * WTM, n0 + wn * WTN, fc, fh);
         return;
     }
     // partial in register order: float4 c of block (i, j) of lane l at ((i TN + j) 4 + c) 64 + l
@@ -682,22 +708,7 @@ gemm_stream_masked_kernel(const float* __restrict__ X, int64_t ldx, const float*
     wait_vmem<0>();
 
     if (ksplit == 1) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int col = n0 + wn * WTN + j * 32 + fc;
-                if (col >= N) continue;
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int row = m0 + wm * WTM + i * 32 + 8 * (e / 4) + 4 * fh + (e % 4);
-                    if (row < M) {
-                        float v = acc[i][j][e];
-                        if (C) v = v - C[(int64_t)row * ldc + col];
-                        Out[(int64_t)row * ldo + col] = v;
-                    }
-                }
-            }
+        store_tile<TM, TN>(acc, C, ldc, Out, ldo, M, N, m0 + wm * WTM, n0 + wn * WTN, fc, fh);
         return;
     }
     float4* mp = reinterpret_cast<float4*>(part) + (((int64_t)tile * ksplit + split) * NW + wave) * (TM * TN * 4 * 64);
