@@ -334,7 +334,7 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], const 
 }
 
 template <int NPL, int BM, int BN, int WGM, int D, int NW = ST_NW, bool TILED = false, int SW = 1>
-__global__ void __launch_bounds__(NW * WAVE)
+__global__ void __launch_bounds__(NW * WAVE, (TILED && NW == 4) ? 2 : 1)
 gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
                    const uint16_t* __restrict__ W, int64_t ldw, const float* __restrict__ C, int64_t ldc,
                    float* __restrict__ Out, int64_t ldo, int M, int N, int K, int mtiles, int ntiles,
@@ -364,7 +364,9 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     const int kt0 = split * kt_per_split;
     const int kt1 = min(kt0 + kt_per_split, ktiles);
     const int nk = kt1 > kt0 ? kt1 - kt0 : 0;
-    const int nloop = (nk + S - 1) / S * S; // whole turns of the ring; tiles past kt1 read zeros
+    // whole turns of the ring in the loop, the last partial turn after it (a test inside the
+    // loop's steps made the compiler wait for every load at each of them); the loads issued
+    // for tiles past the split's last read zeros
 
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (uint32_t)((NPL - 1) * pstride * 2 + (int64_t)M * lda * 2));
     const __amdgpu_buffer_rsrc_t rw =
@@ -498,13 +500,18 @@ gemm_stream_kernel(const uint16_t* __restrict__ A, int64_t lda, int64_t pstride,
     issue(0, std::integral_constant<int, 0>{});
     if constexpr (D > 1) issue(1, std::integral_constant<int, 1>{});
     if constexpr (D > 2) issue(2, std::integral_constant<int, 2>{});
-    for (int t = 0; t < nloop; t += S) {
+    int t = 0;
+    for (; t + S <= nk; t += S) {
         step(t, std::integral_constant<int, 0>{});
         step(t + 1, std::integral_constant<int, 1>{});
         if constexpr (S > 2) step(t + 2, std::integral_constant<int, 2>{});
         if constexpr (S > 3) step(t + 3, std::integral_constant<int, 3>{});
     }
-    wait_vmem<0>(); // the ring's last (zero) tiles have landed before the workgroup ends
+    // the last, partial turn: at most S - 1 tiles, the same count for every wave
+    if (t < nk) step(t, std::integral_constant<int, 0>{});
+    if constexpr (S > 2) if (t + 1 < nk) step(t + 1, std::integral_constant<int, 1>{});
+    if constexpr (S > 3) if (t + 2 < nk) step(t + 2, std::integral_constant<int, 2>{});
+    wait_vmem<0>(); // the loads issued past the last tile (zeros) have landed before the workgroup ends
 
     if (ksplit == 1) {
         store_tile<TM, TN>(acc, C, ldc, Out, ldo, M, N, m0 + wm * WTM, n0 + wn * WTN, fc, fh);
@@ -559,7 +566,6 @@ gemm_stream_masked_kernel(const float* __restrict__ X, int64_t ldx, const float*
     const int kt0 = split * kt_per_split;
     const int kt1 = min(kt0 + kt_per_split, ktiles);
     const int nk = kt1 > kt0 ? kt1 - kt0 : 0;
-    const int nloop = (nk + S - 1) / S * S;
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, (uint32_t)((int64_t)M * ldx * 4));
     const __amdgpu_buffer_rsrc_t re = make_rsrc(E, (uint32_t)((int64_t)M * lde * 4));
@@ -699,12 +705,17 @@ gemm_stream_masked_kernel(const float* __restrict__ X, int64_t ldx, const float*
     load_x(1);
     wait_vmem<(D - 1) * LW + 4>();
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
-    for (int t = 0; t < nloop; t += S) {
+    // whole turns of the ring, then the last partial turn (at most S - 1 tiles)
+    int t = 0;
+    for (; t + S <= nk; t += S) {
         step(t, std::integral_constant<int, 0>{});
         step(t + 1, std::integral_constant<int, 1>{});
         step(t + 2, std::integral_constant<int, 2>{});
         if constexpr (S > 3) step(t + 3, std::integral_constant<int, 3>{});
     }
+    if (t < nk) step(t, std::integral_constant<int, 0>{});
+    if (t + 1 < nk) step(t + 1, std::integral_constant<int, 1>{});
+    if constexpr (S > 3) if (t + 2 < nk) step(t + 2, std::integral_constant<int, 2>{});
     wait_vmem<0>();
 
     if (ksplit == 1) {
