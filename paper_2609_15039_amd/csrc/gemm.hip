@@ -30,20 +30,6 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
 // Epilogue for one accumulator element: the split-K partial or the final value.
-struct TileCtx {
-    int m0, n0, M, N;
-    const float* C; int64_t ldc;
-    float* Out; int64_t ldo;
-};
-
-__device__ __forceinline__ void store_final(const TileCtx& t, int row, int col, float v)
-{
-    if (row < t.M && col < t.N) {
-        if (t.C) v = v - t.C[(int64_t)row * t.ldc + col];
-        t.Out[(int64_t)row * t.ldo + col] = v;
-    }
-}
-
 // Split-K hand-off between the workgroups of one output tile.  Partials are
 // written and read with agent-scope relaxed atomic accesses, which gfx950 performs
 // write-through / coherently (sc1) across the XCDs' L2 caches.  Each wave waits
@@ -897,16 +883,32 @@ gemm_f32_kernel(const float* __restrict__ A, int64_t lda, const void* __restrict
         }
     }
 
-    TileCtx t{m0, n0, M, N, C, ldc, Out, ldo};
     const int erow = 4 * (lane / 16), ecol = lane % 16;
     if (ksplit == 1) {
+        // every C load of the wave tile before the first subtraction (one wait, not one per
+        // element); elements outside M x N load C[0] and store nothing
+        float cv[TM][TN][4];
+        if (C) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int row = m0 + wm * WTM + i * 16 + erow + r, col = n0 + wn * WTN + j * 16 + ecol;
+                        cv[i][j][r] = C[row < M && col < N ? (int64_t)row * ldc + col : 0];
+                    }
+        }
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    store_final(t, m0 + wm * WTM + i * 16 + erow + r, n0 + wn * WTN + j * 16 + ecol, acc[i][j][r]);
+                for (int r = 0; r < 4; ++r) {
+                    const int row = m0 + wm * WTM + i * 16 + erow + r, col = n0 + wn * WTN + j * 16 + ecol;
+                    if (row < M && col < N)
+                        Out[(int64_t)row * ldo + col] = C ? acc[i][j][r] - cv[i][j][r] : acc[i][j][r];
+                }
         return;
     }
     float* mypart = part + ((int64_t)tile * ksplit + split) * (BM * BN);
@@ -1135,9 +1137,15 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
     // 5. epilogue.  Accumulator element r: row 4*(lane/16) + r, column gn.
     const int erow = 4 * (lane / 16);
     if (ksplit == 1) {
-        TileCtx t{0, n0, M, N, C, ldc, Out, ldo};
+        // the four C loads first, then the stores (one wait, not one per element)
+        float cv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (C) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) store_final(t, erow + r, gn, acc[r]);
+            for (int r = 0; r < 4; ++r) cv[r] = C[erow + r < M && gn < N ? (int64_t)(erow + r) * ldc + gn : 0];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            if (erow + r < M && gn < N) Out[(int64_t)(erow + r) * ldo + gn] = C ? acc[r] - cv[r] : acc[r];
         return;
     }
     float* mypart = part + ((int64_t)tile * ksplit + split) * (16 * SK_BN);
