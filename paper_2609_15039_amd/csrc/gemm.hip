@@ -738,21 +738,26 @@ stream_sum_kernel(const float* __restrict__ part, int ksplit, const float* __res
     const int wave = rem / PER_WAVE, e = rem - wave * PER_WAVE;
     const int lane = e % 64, ijc = e / 64, c = ijc % 4, ij = ijc / 4, i = ij / TN, j = ij % TN;
     const int m0 = (tile % mtiles) * BM, n0 = (tile / mtiles) * BN;
-    const float4* src = reinterpret_cast<const float4*>(part) + (((int64_t)tile * ksplit) * NW + wave) * PER_WAVE + e;
     const int wm = wave / WGN, wn = wave % WGN;
     const int col = n0 + wn * WTN + j * 32 + lane % 32;
     const int row0 = m0 + wm * WTM + i * 32 + 8 * c + 4 * (lane / 32);
-    // C first, then every split's partial: all loads in flight together
+    // C first, then every split's partial: all loads in flight together (an element outside
+    // M x N loads C[0], so no load sits behind a branch of its own)
     float cv[4] = {0.f, 0.f, 0.f, 0.f};
-    if (C && col < N) {
+    if (C) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-            if (row0 + r < M) cv[r] = C[(int64_t)(row0 + r) * ldc + col];
+        for (int r = 0; r < 4; ++r) cv[r] = C[row0 + r < M && col < N ? (int64_t)(row0 + r) * ldc + col : 0];
     }
+    // the partials through a buffer resource: a split past ksplit takes an out-of-range offset
+    // and reads zeros, so every load is unconditional (a load behind a branch of its own made
+    // the compiler wait for the loads before it); the host keeps the partials below 2 GB
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(part, (uint32_t)((int64_t)tiles * ksplit * NW * PER_WAVE * 16));
+    const uint32_t off0 = (uint32_t)((((int64_t)tile * ksplit * NW + wave) * PER_WAVE + e) * 16);
     f32x4_t v[ST_MAX_KS];
 #pragma unroll
     for (int q = 0; q < ST_MAX_KS; ++q)
-        v[q] = q < ksplit ? __builtin_bit_cast(f32x4_t, src[(int64_t)q * NW * PER_WAVE]) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        v[q] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                   rp, (int)(q < ksplit ? off0 + (uint32_t)(q * NW * PER_WAVE * 16) : OOB), 0, 0));
     f32x4_t sum = v[0];
 #pragma unroll
     for (int q = 1; q < ST_MAX_KS; ++q)
@@ -2026,7 +2031,8 @@ int launch_gemm(const void* A, int prec, int64_t lda, int64_t pstride, const voi
         // the buffer loads address each operand with 31-bit byte offsets
         const int64_t planes = prec == SPLITEE_PREC_BF16X3 ? 3 : 1;
         const int64_t wbytes = w_type == SPLITEE_BF16_TILED ? (int64_t)splitee::tiled_weights_bytes(N, K) : N * ldw * 2;
-        if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31))
+        if ((planes - 1) * pstride * 2 + M * lda * 2 >= (int64_t(1) << 31) || wbytes >= (int64_t(1) << 31) ||
+            p.part_bytes >= (size_t(1) << 31))
             return SPLITEE_ERR_UNSUPPORTED;
         float* pp = reinterpret_cast<float*>(ws);
 #define ST_LAUNCH(NP, BM_, BN_, WGM_, D_, NW_, T_) hipLaunchKernelGGL((gemm_stream_kernel<NP, BM_, BN_, WGM_, D_, NW_, T_>), grid, dim3(NW_ * WAVE), 0, s, a, lda, pstride, w, ldw, C, ldc, Out, ldo, m, n, k, p.mtiles, p.ntiles, p.ksplit, p.kt_per_split, pp)
@@ -2189,6 +2195,7 @@ int launch_gemm_masked(const float* X, int64_t ldx, const float* eta, int64_t ld
     Plan p = plan_tiled(M, N, K, prec, w_type, allow_split);
     if (p.variant != 24 && p.variant != 25 && p.variant != 26 && p.variant != 27) return SPLITEE_ERR_UNSUPPORTED;
     if (p.ksplit > 1 && ws_bytes < p.counter_bytes + p.part_bytes) return SPLITEE_ERR_WORKSPACE;
+    if (p.part_bytes >= (size_t(1) << 31)) return SPLITEE_ERR_UNSUPPORTED; // the sum kernel's buffer offsets
     float* pp = reinterpret_cast<float*>(ws);
     const uint16_t* w = reinterpret_cast<const uint16_t*>(W);
     dim3 grid((unsigned)(p.mtiles * p.ntiles * p.ksplit));
