@@ -1402,19 +1402,21 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
     const int nchunk = (K + 511) / 512;
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(W, (uint32_t)((int64_t)N * ldw * 2));
 
-    // the masked input of the wave's chunks first, through buffer resources so that the
-    // loads are unconditional (past K they read zeros): a wave's loads complete in order,
-    // so loads issued after W's would hold the conversion until all of W has landed (two
-    // tokens 13% faster on the Qwen3-4B and Llama-3.2-3B projections with this order)
+    // the masked input through buffer resources so that its loads are unconditional (past K
+    // they read zeros); loads issued after W's would hold its conversion until all of W had
+    // landed (two tokens 13% faster on the Qwen3-4B and Llama-3.2-3B projections with the
+    // masked input first)
     const int MRr = MR;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(MASK ? (const void*)src.X : (const void*)src.A,
                                                 MASK ? (uint32_t)((int64_t)MRr * src.ldx * 4)
                                                      : (uint32_t)(((NPL - 1) * src.pstride + (int64_t)MRr * src.lda) * 2));
     const __amdgpu_buffer_rsrc_t re = make_rsrc(MASK ? (const void*)src.eta : (const void*)src.A,
                                                 MASK ? (uint32_t)((int64_t)MRr * src.ld_eta * 4) : 0u);
-    float x[CH][MR][8];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
+    // raw masked-input words of chunk c, row m: X and eta (two 16-byte loads each) or the
+    // NPL bfloat16 planes
+    constexpr int XW = MASK ? 4 : NPL;
+    uint4 xr[CH][MR][XW];
+    auto load_x = [&](int c) {
         const int j = wave + GV_WAVES * c, k = 512 * j + 8 * lane;
         const bool ok = j < nchunk && k < K;
 #pragma unroll
@@ -1422,10 +1424,24 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
             if (MASK) {
                 const uint32_t xo = ok ? (uint32_t)(((int64_t)m * src.ldx + k) * 4) : OOB;
                 const uint32_t eo = ok ? (uint32_t)(((int64_t)m * src.ld_eta + k) * 4) : OOB;
-                const uint4 xv[2] = {load16(rx, xo), load16(rx, ok ? xo + 16 : OOB)};
-                const uint4 ev[2] = {load16(re, eo), load16(re, ok ? eo + 16 : OOB)};
-                const float* a = reinterpret_cast<const float*>(xv);
-                const float* e = reinterpret_cast<const float*>(ev);
+                xr[c][m][0] = load16(rx, xo);
+                xr[c][m][1] = load16(rx, ok ? xo + 16 : OOB);
+                xr[c][m][2] = load16(re, eo);
+                xr[c][m][3] = load16(re, ok ? eo + 16 : OOB);
+            } else {
+#pragma unroll
+                for (int p = 0; p < NPL; ++p)
+                    xr[c][m][p] = load16(rx, ok ? (uint32_t)((p * src.pstride + (int64_t)m * src.lda + k) * 2) : OOB);
+            }
+        }
+    };
+    float x[CH][MR][8];
+    auto convert_x = [&](int c) {
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+            if (MASK) {
+                const float* a = reinterpret_cast<const float*>(&xr[c][m][0]);
+                const float* e = reinterpret_cast<const float*>(&xr[c][m][2]);
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     float v = a[q] + e[q];
@@ -1433,16 +1449,12 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
                     x[c][m][q] = v;
                 }
             } else {
-                uint4 pl[NPL];
-#pragma unroll
-                for (int p = 0; p < NPL; ++p)
-                    pl[p] = load16(rx, ok ? (uint32_t)((p * src.pstride + (int64_t)m * src.lda + k) * 2) : OOB);
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     float v = 0.f;
 #pragma unroll
                     for (int p = 0; p < NPL; ++p) {
-                        const uint32_t wd = reinterpret_cast<const uint32_t*>(&pl[p])[q / 2];
+                        const uint32_t wd = reinterpret_cast<const uint32_t*>(&xr[c][m][p])[q / 2];
                         const float t = splitee::bf16_bits_to_f32((q & 1) ? (wd >> 16) : (wd & 0xFFFFu));
                         v = p == 0 ? t : v + t; // hi + mid, then + lo: exact
                     }
@@ -1450,18 +1462,33 @@ gemv_split_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const 
                 }
             }
         }
-    }
-
-    // then every W load of the wave, all in flight at once
+    };
     uint4 wv[CH][GS_ROWS];
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
+    auto load_w = [&](int c) {
         const int j = wave + GV_WAVES * c, k = 512 * j + 8 * lane;
 #pragma unroll
         for (int r = 0; r < GS_ROWS; ++r) {
             const bool ok = j < nchunk && k < K && n0 + r < N;
             wv[c][r] = load16(rw, ok ? (uint32_t)(((int64_t)(n0 + r) * ldw + k) * 2) : OOB);
         }
+    };
+    // the masked input's loads first (a wave's loads complete in order, so the conversion
+    // never waits for W), then, where the raw input words and all of W fit the registers of
+    // four waves per SIMD, every W load before the conversion, so that the two latencies
+    // overlap; otherwise the conversion first, then every W load
+    constexpr bool EARLY_W = CH * (GS_ROWS + MR * XW) * 4 <= 96;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) load_x(c);
+    if constexpr (EARLY_W) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) load_w(c);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) convert_x(c);
+    } else {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) convert_x(c);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) load_w(c);
     }
     float acc[MR][GS_ROWS];
 #pragma unroll
