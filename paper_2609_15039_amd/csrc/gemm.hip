@@ -29,22 +29,17 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// Epilogue for one accumulator element: the split-K partial or the final value.
 // Split-K hand-off between the workgroups of one output tile.  Partials are
-// written and read with agent-scope relaxed atomic accesses, which gfx950 performs
-// write-through / coherently (sc1) across the XCDs' L2 caches.  Each wave waits
-// for its partial stores to complete before the workgroup bumps the tile
-// counter, so the workgroup that sees the count reach ksplit-1 reads complete
-// partials.  This is the ordering of an agent-scope release/acquire pair
-// without its whole-L2 write-back and invalidate, which only non-coherent
-// stores need.
+// written with agent-scope relaxed atomic stores (or sc1 buffer stores) and read
+// with sc1 buffer loads, which gfx950 performs write-through / coherently across
+// the XCDs' L2 caches.  Each wave waits for its partial stores to complete before
+// the workgroup bumps the tile counter, so the workgroup that sees the count reach
+// ksplit-1 reads complete partials.  This is the ordering of an agent-scope
+// release/acquire pair without its whole-L2 write-back and invalidate, which only
+// non-coherent stores need.
 __device__ __forceinline__ void store_partial(float* p, float v)
 {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_partial(const float* p)
-{
-    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Returns true in the last-arriving workgroup of the tile (all its threads),
@@ -1160,11 +1155,15 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
     if (!splitk_arrive(counters + tile, ksplit, reinterpret_cast<unsigned*>(sa))) return;
 
     // last workgroup: thread t sums the float4 at row t / 16, columns 4 * (t % 16)..+3
-    // over the splits in split order, eight splits' loads in flight at a time
+    // over the splits in split order, eight splits' loads in flight at a time; its C
+    // float4 is loaded first, so that it arrives with the partials
     const int row = tid / 16, c4 = (tid % 16) * 4;
     if (row < M) {
         const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
             part + (int64_t)tile * ksplit * (16 * SK_BN), (short)0, ksplit * 16 * SK_BN * 4, 0x00020000);
+        const int gc = n0 + c4;
+        f32x4_t cv = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        if (C && gc + 4 <= N) cv = __builtin_bit_cast(f32x4_t, *reinterpret_cast<const float4*>(C + (int64_t)row * ldc + gc));
         f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
         for (int q0 = 0; q0 < ksplit; q0 += 8) {
             f32x4_t v[8];
@@ -1177,9 +1176,8 @@ skinny_kernel(SkSrc src, const uint16_t* __restrict__ W, int64_t ldw, const floa
             for (int i = 0; i < 8; ++i)
                 if (q0 + i < ksplit) sum = (q0 + i == 0) ? v[i] : sum + v[i];
         }
-        const int gc = n0 + c4;
         if (gc + 4 <= N) {
-            if (C) sum -= __builtin_bit_cast(f32x4_t, *reinterpret_cast<const float4*>(C + (int64_t)row * ldc + gc));
+            if (C) sum -= cv;
             *reinterpret_cast<float4*>(Out + (int64_t)row * ldo + gc) = __builtin_bit_cast(float4, sum);
         } else {
             for (int e = 0; e < 4 && gc + e < N; ++e) {
@@ -1674,12 +1672,22 @@ gemv_tiled_kernel(SkSrc src, const uint16_t* __restrict__ W, const float* __rest
     if (owner) store_partial(&part[(((int64_t)cb * ksplit + split) * MR + om) * 32 + orow], y);
     if (!splitk_arrive(counters + cb, ksplit, &flag)) return;
     if (owner) {
+        // C first, then the splits' partials eight at a time (agent-coherent buffer loads; a
+        // split past ksplit reads zeros and is not added), summed in split order
+        const float cv = C && col < N ? C[(int64_t)om * ldc + col] : 0.f;
+        const __amdgpu_buffer_rsrc_t rp = make_rsrc(part + (int64_t)cb * ksplit * MR * 32, (uint32_t)(ksplit * MR * 32 * 4));
         float sum = 0.f;
-        for (int q = 0; q < ksplit; ++q) {
-            const float v = load_partial(&part[(((int64_t)cb * ksplit + q) * MR + om) * 32 + orow]);
-            sum = q == 0 ? v : sum + v;
+        for (int q0 = 0; q0 < ksplit; q0 += 8) {
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                v[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                           rp, (int)(q0 + i < ksplit ? (uint32_t)((((q0 + i) * MR + om) * 32 + orow) * 4) : OOB_OFF), 0, SC1));
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (q0 + i < ksplit) sum = (q0 + i == 0) ? v[i] : sum + v[i];
         }
-        if (col < N) Out[(int64_t)om * ldo + col] = C ? sum - C[(int64_t)om * ldc + col] : sum;
+        if (col < N) Out[(int64_t)om * ldo + col] = C ? sum - cv : sum;
     }
     if (tid == 0) splitk_reset(counters + cb);
 }
